@@ -1,0 +1,465 @@
+"""Pins of the CPU oracle against what the paper and the mathematics fix.
+
+Each test checks the oracle against something other than itself: a closed
+form, an invariant the paper states, a special case that reduces to a
+library routine, or brute force on tiny inputs.
+"""
+
+import math
+
+import numpy as np
+import pytest
+from scipy import stats
+from sklearn.metrics import mutual_info_score
+
+from oracle import starkv_oracle as O
+
+
+def rng(seed):
+    return np.random.default_rng(seed)
+
+
+# ----------------------------------------------------------------- Eq. A_raw
+
+def test_window_rows_sum_to_one():
+    """Each window row is a softmax over the past keys, so summing A_raw over
+    tokens gives W for every head (sec. 3.3)."""
+    r = rng(1)
+    Q = r.standard_normal((6, 5, 16))
+    K = r.standard_normal((3, 40, 16)) * 3.0
+    A = O.window_attention_mass(Q, K)
+    assert A.shape == (6, 40)
+    np.testing.assert_allclose(A.sum(axis=1), 5.0, rtol=1e-13)
+    assert (A > 0).all()
+
+
+def test_two_key_closed_form_checks_sqrt_d_scaling():
+    """Two keys, one query: p = 1 / (1 + e^{-(x1 - x2)}) with x = q.k/sqrt(d)."""
+    d = 4
+    Q = np.zeros((1, 1, d))
+    Q[0, 0, 0] = 2.0
+    K = np.zeros((1, 2, d))
+    K[0, 0, 0] = 1.0          # x1 = 2 * 1 / sqrt(4) = 1, x2 = 0
+    A = O.window_attention_mass(Q, K)
+    p1 = 1.0 / (1.0 + math.exp(-1.0))
+    np.testing.assert_allclose(A[0], [p1, 1.0 - p1], rtol=1e-14)
+
+
+def test_zero_queries_give_uniform_mass():
+    Q = np.zeros((2, 7, 8))
+    K = rng(2).standard_normal((1, 13, 8))
+    A = O.window_attention_mass(Q, K)
+    np.testing.assert_allclose(A, 7.0 / 13.0, rtol=1e-14)
+
+
+def test_gqa_head_to_group_map():
+    """g(h) = floor(h G / H): with H=6, G=3 heads {0,1}->0, {2,3}->1, {4,5}->2
+    (sec. 3.1).  Changing group 1's keys moves heads 2 and 3 only."""
+    r = rng(3)
+    Q = r.standard_normal((6, 2, 8))
+    K = r.standard_normal((3, 9, 8))
+    A0 = O.window_attention_mass(Q, K)
+    K2 = K.copy()
+    K2[1] = r.standard_normal((9, 8))
+    A1 = O.window_attention_mass(Q, K2)
+    changed = [not np.allclose(A0[h], A1[h]) for h in range(6)]
+    assert changed == [False, False, True, True, False, False]
+
+
+def test_window_sum_decomposes_over_queries():
+    r = rng(4)
+    Q = r.standard_normal((2, 4, 8))
+    K = r.standard_normal((1, 11, 8))
+    A = O.window_attention_mass(Q, K)
+    parts = sum(O.window_attention_mass(Q[:, i:i + 1], K) for i in range(4))
+    np.testing.assert_allclose(A, parts, rtol=1e-13)
+
+
+def test_window_mass_brute_force_tiny():
+    """Scalar loops over a tiny case: H=2, G=1, W=2, L_p=3, d=2."""
+    r = rng(5)
+    Q = r.standard_normal((2, 2, 2))
+    K = r.standard_normal((1, 3, 2))
+    want = np.zeros((2, 3))
+    for h in range(2):
+        for i in range(2):
+            logits = [sum(Q[h, i, j] * K[0, t, j] for j in range(2)) / math.sqrt(2)
+                      for t in range(3)]
+            z = sum(math.exp(x) for x in logits)
+            for t in range(3):
+                want[h, t] += math.exp(logits[t]) / z
+    np.testing.assert_allclose(O.window_attention_mass(Q, K), want, rtol=1e-13)
+
+
+# ------------------------------------------------------------ AvgPool1D
+
+def test_pool_impulse_response():
+    x = np.zeros((1, 20))
+    x[0, 10] = 1.0
+    y = O.avg_pool1d(x, 5)
+    want = np.zeros(20)
+    want[8:13] = 0.2
+    np.testing.assert_allclose(y[0], want, atol=1e-16)
+    assert y.sum() == pytest.approx(1.0, abs=1e-15)
+
+
+def test_pool_constant_edges_count_padding():
+    y = O.avg_pool1d(np.full((1, 10), 3.0), 5)
+    np.testing.assert_allclose(y[0], [1.8, 2.4, 3, 3, 3, 3, 3, 3, 2.4, 1.8], rtol=1e-15)
+
+
+def test_pool_width_one_is_identity():
+    x = rng(6).random((3, 17))
+    np.testing.assert_array_equal(O.avg_pool1d(x, 1), x)
+
+
+# ------------------------------------------------------------ Eq. base_score
+
+def test_group_scores_reduce_to_mha():
+    """G = H recovers standard multi-head attention: S = A (sec. 3.1)."""
+    A = rng(7).random((4, 9))
+    np.testing.assert_allclose(O.group_scores(A, 4), A, rtol=1e-15)
+
+
+def test_group_scores_are_head_means():
+    A = np.repeat(np.array([[1.0], [2.0], [3.0], [4.0]]), 5, axis=1)
+    S = O.group_scores(A, 2)
+    np.testing.assert_allclose(S, [[1.5] * 5, [3.5] * 5], rtol=1e-15)
+
+
+def test_base_score_single_group_and_ties():
+    S = rng(8).random((1, 6))
+    sbar, gstar = O.base_score(S)
+    np.testing.assert_array_equal(sbar, S[0])
+    assert (gstar == 0).all()
+    S2 = np.array([[1.0, 2.0, 5.0], [3.0, 2.0, 1.0], [3.0, 1.0, 5.0]])
+    sbar2, g2 = O.base_score(S2)
+    np.testing.assert_allclose(sbar2, [7 / 3, 5 / 3, 11 / 3], rtol=1e-15)
+    assert list(g2) == [1, 0, 0]      # ties keep the lowest group
+
+
+# ------------------------------------------------------------ RankBin / MI
+
+def test_rank_bins_match_ordinal_ranks_and_equal_frequency():
+    r = rng(9)
+    v = r.random(103)
+    v[10] = v[20] = v[30]          # ties resolved by index
+    b = O.rank_bins(v, 8)
+    ordinal = stats.rankdata(v, method="ordinal") - 1
+    np.testing.assert_array_equal(b, ordinal * 8 // 103)
+    counts = np.bincount(b, minlength=8)
+    assert set(counts) <= {103 // 8, 103 // 8 + 1}
+    assert b[10] <= b[20] <= b[30]
+
+
+def test_rank_bins_all_equal_follow_index():
+    b = O.rank_bins(np.full(10, 0.5), 4)
+    np.testing.assert_array_equal(b, (np.arange(10) * 4) // 10)
+
+
+def test_rank_bins_invariant_to_monotone_transform():
+    v = rng(10).random(50)
+    np.testing.assert_array_equal(O.rank_bins(v, 5), O.rank_bins(np.exp(3 * v) + 7, 5))
+
+
+def _grid(nr, nc):
+    t = np.arange(nr * nc)
+    return t // nc, t % nc
+
+
+def test_mi_zero_for_factorised_construction():
+    """16x16 tokens on an 8x8 grid: four tokens per cell, one per 2x2
+    sub-position.  Values ordered by sub-position make every cell hold one
+    token of each of the K=4 bins, so p(b,c) = p(b) p(c) and MI = 0."""
+    r, c = _grid(16, 16)
+    cell = O.spatial_cells(r, c, 16, 16, 8)
+    sub = (r % 2) * 2 + (c % 2)
+    values = sub * 1000.0 + cell
+    b = O.rank_bins(values, 4)
+    assert O.plugin_mi(b, cell, 4, 64) == 0.0
+
+
+def test_constant_attention_is_not_mi_zero_under_index_ties():
+    """Constant values rank by index, so bins follow raster order and share
+    information with the rows: MI > 0 (the reason the zero case above is
+    built from sub-positions)."""
+    r, c = _grid(16, 16)
+    cell = O.spatial_cells(r, c, 16, 16, 8)
+    b = O.rank_bins(np.ones(256), 4)
+    assert O.plugin_mi(b, cell, 4, 64) > 0.1
+
+
+def test_mi_maximum_ln_k():
+    """K = M^2 bins, equal cells, values increasing with the cell id: bins
+    equal cells and MI = ln K."""
+    r, c = _grid(4, 4)
+    cell = O.spatial_cells(r, c, 4, 4, 2)
+    values = cell * 10.0 + np.arange(16) * 0.01
+    b = O.rank_bins(values, 4)
+    assert O.plugin_mi(b, cell, 4, 4) == pytest.approx(math.log(4), rel=1e-14)
+
+
+@pytest.mark.parametrize("seed", [11, 12, 13])
+def test_mi_matches_sklearn_and_entropy_identity(seed):
+    r = rng(seed)
+    nr, nc = 13, 17
+    rr, cc = _grid(nr, nc)
+    cell = O.spatial_cells(rr, cc, nr, nc, 4)
+    values = r.random(nr * nc) + 0.5 * (cc > nc // 2)
+    b = O.rank_bins(values, 5)
+    mi = O.plugin_mi(b, cell, 5, 16)
+    assert mi == pytest.approx(mutual_info_score(b, cell), rel=1e-12, abs=1e-14)
+    joint = np.zeros((5, 16))
+    np.add.at(joint, (b, cell), 1)
+    h_b = stats.entropy(joint.sum(1))
+    h_c = stats.entropy(joint.sum(0))
+    h_bc = stats.entropy(joint.ravel())
+    assert mi == pytest.approx(h_b + h_c - h_bc, rel=1e-12, abs=1e-14)
+    assert 0.0 <= mi <= min(math.log(5), h_c) + 1e-12
+
+
+def test_spatial_cells_per_frame_grid():
+    r, c = _grid(39, 69)
+    cell = O.spatial_cells(r, c, 39, 69, 8)
+    assert cell.min() == 0 and cell.max() == 63
+    assert cell[0] == 0 and cell[68] == 7 and cell[-1] == 63
+    assert cell[38 * 69] == 56
+
+
+def test_mi_empty_token_set():
+    assert O.plugin_mi(np.zeros(0, dtype=int), np.zeros(0, dtype=int), 8, 64) == 0.0
+
+
+# ------------------------------------------------------------ subspace prior
+
+def test_prior_uniform_when_mi_equal():
+    w = O.mi_prior(np.full(4, 0.3), 1.0, 1e-8)
+    np.testing.assert_allclose(w, 0.25, rtol=1e-15)
+    # G w_{g*} averages to one: beta = (1 - lam) + lam G w = 1 (sec. 3.4)
+    lam = 0.5
+    np.testing.assert_allclose((1 - lam) + lam * 4 * w, 1.0, rtol=1e-15)
+
+
+def test_prior_two_groups_closed_form():
+    eps = 1e-8
+    w = O.mi_prior(np.array([0.2, 1.2]), 2.0, eps)
+    m1 = 1.0 / (1.0 + eps)
+    want1 = math.exp(m1 / 2) / (1 + math.exp(m1 / 2))
+    np.testing.assert_allclose(w, [1 - want1, want1], rtol=1e-14)
+
+
+def test_prior_sums_to_one_and_is_order_preserving():
+    mi = rng(14).random(6)
+    w = O.mi_prior(mi, 1.0, 1e-8)
+    assert w.sum() == pytest.approx(1.0, abs=1e-15)
+    assert list(np.argsort(w)) == list(np.argsort(mi))
+
+
+def test_lambda_schedule_values():
+    vals = [O.lambda_schedule(n, 0.5, 5, 10) for n in range(1, 21)]
+    assert vals[:5] == [0.0] * 5
+    assert vals[5] == pytest.approx(0.05)
+    assert vals[9] == pytest.approx(0.25)
+    assert vals[14:] == [0.5] * 6
+    assert O.lambda_schedule(1, 0.5, 0, 0) == 0.5
+
+
+def test_mi_ema_closed_form():
+    """A constant MI c for n steps from zero gives (1 - rho^n) c."""
+    mi_bar = np.zeros(2)
+    c = np.array([0.3, 0.7])
+    for _ in range(7):
+        mi_bar = 0.9 * mi_bar + 0.1 * c
+    np.testing.assert_allclose(mi_bar, (1 - 0.9 ** 7) * c, rtol=1e-14)
+
+
+# ------------------------------------------------------------ stability
+
+def test_stability_same_row_twice():
+    s = rng(15).random((3, 20))
+    phi1, m1 = O.stability(s, np.zeros((3, 20)), 0.9, 1e-8)
+    np.testing.assert_array_equal(phi1, 0.0)
+    np.testing.assert_allclose(m1, 0.1 * s, rtol=1e-15)
+    phi2, _ = O.stability(s, m1, 0.9, 1e-8)
+    np.testing.assert_allclose(phi2, 1.0, atol=1e-7)
+
+
+def test_stability_uses_old_mean():
+    """phi comes from m before the update: orthogonal rows give phi = 0."""
+    s1 = np.array([[1.0, 0.0, 2.0, 0.0]])
+    s2 = np.array([[0.0, 3.0, 0.0, 1.0]])
+    _, m1 = O.stability(s1, np.zeros((1, 4)), 0.9, 1e-8)
+    phi2, m2 = O.stability(s2, m1, 0.9, 1e-8)
+    assert phi2[0] == 0.0
+    np.testing.assert_allclose(m2, 0.09 * s1 + 0.1 * s2, rtol=1e-15)
+
+
+def test_stability_ema_closed_form_and_range():
+    s = rng(16).random((2, 8))
+    m = np.zeros((2, 8))
+    for _ in range(5):
+        phi, m = O.stability(s, m, 0.8, 1e-8)
+    np.testing.assert_allclose(m, (1 - 0.8 ** 5) * s, rtol=1e-14)
+    assert ((phi >= 0) & (phi <= 1 + 1e-12)).all()
+
+
+# ------------------------------------------------------------ discount
+
+def test_discount_closed_form_and_special_cases():
+    is_vis = np.array([True, True, True, False, True])
+    frame = np.array([1, 2, 3, 0, 1])
+    phi_t = np.array([0.5, 1.0, 0.3, 0.9, 0.0])
+    D = O.temporal_discount(is_vis, frame, 3, phi_t, 0.2, 0.1)
+    want0 = 0.1 + 0.9 * math.exp(-0.2 * 2 * 0.5)
+    want1 = 0.1 + 0.9 * math.exp(-0.2 * 1 * 1.0)
+    np.testing.assert_allclose(D, [want0, want1, 1.0, 1.0, 1.0], rtol=1e-15)
+    # delta = 0 and a single frame both give D = 1
+    np.testing.assert_array_equal(
+        O.temporal_discount(is_vis, frame, 3, phi_t, 0.0, 0.1), 1.0)
+    np.testing.assert_array_equal(
+        O.temporal_discount(is_vis, np.full(5, 3), 3, phi_t, 0.2, 0.1), 1.0)
+    far = O.temporal_discount(np.array([True]), np.array([0]), 10 ** 6,
+                              np.array([1.0]), 0.2, 0.1)
+    assert far[0] == pytest.approx(0.1, abs=1e-15)
+
+
+# ------------------------------------------------------------ AEB
+
+def test_entropy_uniform_and_one_hot():
+    h, T = O.entropy_temperature(np.full(100, 0.37), 0.75, 1.25, 1e-8)
+    assert h == pytest.approx(1.0, abs=1e-6)
+    assert T == pytest.approx(1.25, abs=1e-6)
+    one = np.zeros(100)
+    one[17] = 2.0
+    h0, T0 = O.entropy_temperature(one, 0.75, 1.25, 1e-8)
+    assert h0 == pytest.approx(0.0, abs=1e-7)
+    assert T0 == pytest.approx(0.75, abs=1e-7)
+
+
+def test_entropy_matches_scipy():
+    x = rng(17).random(3000) ** 3
+    h0, _ = O.entropy_temperature(x, 0.75, 1.25, 0.0)
+    assert h0 == pytest.approx(stats.entropy(x) / math.log(3000), rel=1e-12)
+    h, _ = O.entropy_temperature(x, 0.75, 1.25, 1e-8)
+    # eps inside the log moves H^ by at most L eps / ln L
+    assert abs(h - h0) <= 3000 * 1e-8 / math.log(3000) + 1e-12
+    assert 0.0 <= h <= 1.0
+
+
+def test_entropy_single_token():
+    assert O.entropy_temperature(np.array([1.0]), 0.5, 1.5, 1e-8) == (0.0, 0.5)
+
+
+# ------------------------------------------------------------ final score
+
+def test_unit_temperature_leaves_scores_unchanged():
+    r = rng(18)
+    sbar, beta, D = r.random(50), r.random(50) + 0.5, r.random(50)
+    s_f, s = O.final_score(sbar, beta, D, 1.0)
+    np.testing.assert_array_equal(s, s_f)
+    np.testing.assert_array_equal(s_f, sbar * beta * D)
+
+
+def test_power_sharpening_closed_form():
+    s_f, s = O.final_score(np.array([0.25, 4.0, -1.0]), np.ones(3), np.ones(3), 2.0)
+    np.testing.assert_allclose(s, [0.5, 2.0, 0.0], rtol=1e-15)
+    _, s2 = O.final_score(np.array([0.25, 4.0]), np.ones(2), np.ones(2), 0.5)
+    np.testing.assert_allclose(s2, [0.0625, 16.0], rtol=1e-15)
+
+
+# ------------------------------------------------------------ selection
+
+def test_topb_brute_force_and_ties():
+    r = rng(19)
+    s = np.round(r.random(30), 1)     # many ties
+    for B in [0, 1, 7, 15, 29, 30]:
+        I = O.topb_select(s, B)
+        brute = sorted(sorted(range(30), key=lambda t: (-s[t], t))[:B])
+        assert list(I) == brute
+        assert len(I) == B
+        assert all(I[i] < I[i + 1] for i in range(len(I) - 1))
+
+
+def test_topb_invariant_under_temperature():
+    """x^(1/T) is increasing, so the hard top-B set does not depend on T."""
+    r = rng(20)
+    s_f = r.random(200)
+    _, s = O.final_score(s_f, np.ones(200), np.ones(200), 0.8)
+    np.testing.assert_array_equal(O.topb_select(s, 40), O.topb_select(s_f, 40))
+
+
+def test_gather_compact_is_row_copy():
+    r = rng(21)
+    K = r.integers(0, 65535, size=(2, 12, 4)).astype(np.uint16)
+    V = r.integers(0, 65535, size=(2, 12, 4)).astype(np.uint16)
+    I = np.array([1, 4, 5])
+    Ko, Vo = O.gather_compact(K, V, I, 10, 3)
+    np.testing.assert_array_equal(Ko, K[:, [1, 4, 5, 7, 8, 9]])
+    np.testing.assert_array_equal(Vo, V[:, [1, 4, 5, 7, 8, 9]])
+    assert Ko.dtype == np.uint16
+
+
+# ------------------------------------------------------------ whole layer
+
+def _tiny_layer(seed, n_frames=1, H=4, G=2, d=8, nr=4, nc=5, text=6, W=3):
+    r = rng(seed)
+    nf = nr * nc
+    L = n_frames * nf + text
+    spans = [((f - 1) * nf, nr, nc, f) for f in range(1, n_frames + 1)]
+    Q = r.standard_normal((H, W, d))
+    K = r.standard_normal((G, L, d))
+    V = r.standard_normal((G, L, d))
+    return Q, K, V, L, W, spans
+
+
+def test_base_reduction():
+    """lambda = 0, one frame and T_min = T_max = 1 reduce STaR-KV to the
+    'Base' ablation row: s = sbar and a global top-B of the GQA-mean score."""
+    Q, K, V, L, W, spans = _tiny_layer(22)
+    p = O.Params(lam=0.0, t_min=1.0, t_max=1.0)
+    out, _ = O.compress_layer(Q, K, V, L, W, spans, 1, 7, p, O.LayerState(2))
+    np.testing.assert_array_equal(out["s"], out["sbar"])
+    np.testing.assert_array_equal(out["D"], 1.0)
+    np.testing.assert_array_equal(out["beta"], 1.0)
+    assert list(out["I"]) == sorted(np.argsort(-out["sbar"], kind="stable")[:7])
+
+
+def test_layer_state_across_steps():
+    """Two steps: the counter advances, MI_bar follows the EMA recursion from
+    zero, phi is 0 on the first step, and frame-1 tokens get discounted."""
+    p = O.Params(n_warmup=0, n_ramp=0)
+    st = O.LayerState(2)
+    Q, K, V, L, W, spans = _tiny_layer(23, n_frames=2)
+    nf = 20
+    spans1 = spans[:1]
+    L1 = nf + 6
+    K1 = np.concatenate([K[:, :nf], K[:, 2 * nf:]], axis=1)
+    V1 = np.concatenate([V[:, :nf], V[:, 2 * nf:]], axis=1)
+    o1, st = O.compress_layer(Q, K1, V1, L1, W, spans1, 1, 5, p, st)
+    assert st.n == 1
+    np.testing.assert_array_equal(o1["phi"], 0.0)
+    np.testing.assert_allclose(o1["mi_bar"], 0.1 * o1["mi"], rtol=1e-15)
+    o2, st = O.compress_layer(Q, K, V, L, W, spans, 2, 9, p, st)
+    assert st.n == 2
+    np.testing.assert_allclose(o2["mi_bar"], 0.09 * o1["mi"] + 0.1 * o2["mi"], rtol=1e-14)
+    assert ((o2["phi"] > 0) & (o2["phi"] <= 1)).all()
+    old = np.arange(nf)
+    want = 0.1 + 0.9 * np.exp(-0.2 * 1 * o2["phi"][o2["gstar"][old]])
+    np.testing.assert_allclose(o2["D"][old], want, rtol=1e-14)
+    np.testing.assert_array_equal(o2["D"][nf:], 1.0)
+    lam = 0.5
+    np.testing.assert_allclose(
+        o2["beta"], (1 - lam) + lam * 2 * o2["w"][o2["gstar"]], rtol=1e-15)
+    assert len(o2["I"]) == 9
+    assert o2["K_out"].shape == (2, 9 + W, 8)
+
+
+def test_frame_size_change_resets_stability():
+    p = O.Params()
+    st = O.LayerState(2)
+    Q, K, V, L, W, spans = _tiny_layer(24)
+    _, st = O.compress_layer(Q, K, V, L, W, spans, 1, 4, p, st)
+    Q2, K2, V2, L2, W2, spans2 = _tiny_layer(25, nr=3, nc=5)
+    o, st = O.compress_layer(Q2, K2, V2, L2, W2, spans2, 1, 4, p, st)
+    np.testing.assert_array_equal(o["phi"], 0.0)
+    assert st.m.shape == (2, 15)
