@@ -339,12 +339,14 @@ def visual_metadata(spans, L_p: int):
 
 
 def compress_layer(Q, K, V, L: int, W: int, spans, F: int, B: int,
-                   params: Params, state: LayerState):
+                   params: Params, state: LayerState, copy_rows=None):
     """One layer of one trajectory step, in the order of Algorithm 1.
 
-    Q: [H, W, d] window queries; K, V: [G, >=L, d] cache (token order);
-    spans: visual spans inside the L_p past tokens; F: current frame; B:
-    budget.  Returns (out, new_state), out holding every intermediate.
+    Q: [H, W, d] window queries; K, V: [G, >=L, d] cache (token order), as
+    real values; spans: visual spans inside the L_p past tokens; F: current
+    frame; B: budget.  copy_rows: optional (K_rows, V_rows) arrays the compacted
+    cache copies its rows from (e.g. the stored bf16 bit patterns); default
+    (K, V).  Returns (out, new_state), out holding every intermediate.
     """
     p = params
     Qf = np.asarray(Q, dtype=np.float64)
@@ -394,7 +396,8 @@ def compress_layer(Q, K, V, L: int, W: int, spans, F: int, B: int,
     # Fusion and selection (sec. 3.2, 3.7)
     s_f, s = final_score(sbar, beta, D, T)
     I = topb_select(s, B)
-    K_out, V_out = gather_compact(K, V, I, L, W)
+    K_rows, V_rows = copy_rows if copy_rows is not None else (K, V)
+    K_out, V_out = gather_compact(K_rows, V_rows, I, L, W)
 
     new_state = LayerState(G, mi_bar, m_new, n)
     out = dict(A_raw=A_raw, A=A, S=S, sbar=sbar, gstar=gstar, mi=mi,

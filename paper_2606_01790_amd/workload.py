@@ -235,6 +235,19 @@ class Trajectory:
         return np.concatenate(ks, axis=1), np.concatenate(vs, axis=1)
 
 
+def random_case(seed: int, n_layers: int, H: int, G: int, d: int, L_cap: int,
+                W: int, dtype: str, scale: float = 1.0):
+    """Plain seeded N(0, scale^2) Q [n_layers, H, W, d] and K, V
+    [n_layers, G, L_cap, d] in storage form (edge-case tests)."""
+    r = np.random.default_rng([seed, 77])
+    Q = (r.standard_normal((n_layers, H, W, d), dtype=np.float32) * np.float32(scale))
+    K = (r.standard_normal((n_layers, G, L_cap, d), dtype=np.float32) * np.float32(scale))
+    V = r.standard_normal((n_layers, G, L_cap, d), dtype=np.float32)
+    if dtype == "bf16":
+        return f32_to_bf16_bits(Q), f32_to_bf16_bits(K), f32_to_bf16_bits(V)
+    return Q, K, V
+
+
 # --------------------------------------------------------------------------
 # algorithmic traffic and flop counts (what the measurement credits)
 # --------------------------------------------------------------------------

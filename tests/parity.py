@@ -1,0 +1,135 @@
+"""GPU-vs-oracle comparison helpers for the parity tests.
+
+The bar (per layer and step):
+  * S, sbar, s in float32: within 1e-3 relative of the oracle (scores > 0);
+  * g*: exact except where the oracle's two best groups are within 1e-5
+    relative (both are valid argmaxes up to rounding);
+  * idx: the GPU set equals the oracle set except for tokens whose oracle
+    score lies within 1e-3 * s_(B) of the B-th oracle score s_(B);
+  * K', V': bit-exact copies;
+  * MI, w, phi, H^, T: within 1e-4 absolute stage-wise (the oracle applied to
+    the GPU's own inputs of that stage), and within the looser end-to-end
+    bounds below when the oracle runs from the raw inputs.
+Decisions (rank bins, top-B) are re-taken by the oracle on the GPU's own
+float32 values for the stage-wise checks, so both sides decide on identical
+numbers.
+"""
+
+from __future__ import annotations
+
+import numpy as np
+
+from oracle import starkv_oracle as O
+from paper_2606_01790_amd import starkv as sk
+
+REL = 1e-3
+
+
+def oracle_params(p: sk.Params) -> O.Params:
+    return O.Params(lam=float(p.lam), n_warmup=int(p.n_warmup), n_ramp=int(p.n_ramp),
+                    rho_mi=float(p.rho_mi), tau=float(p.tau), rho_t=float(p.rho_t),
+                    delta=float(p.delta), d_min=float(p.d_min), t_min=float(p.t_min),
+                    t_max=float(p.t_max), n_bins=int(p.n_bins), grid=int(p.grid),
+                    pool_kernel=int(p.pool_kernel), eps=float(p.eps))
+
+
+def max_rel(a, b):
+    a = np.asarray(a, np.float64)
+    b = np.asarray(b, np.float64)
+    return float(np.max(np.abs(a - b) / np.maximum(np.abs(b), 1e-30))) if a.size else 0.0
+
+
+def scal_fields(scal: np.ndarray, G: int) -> dict:
+    return dict(mi=scal[0:G], mi_bar=scal[G:2 * G], w=scal[2 * G:3 * G],
+                phi=scal[3 * G:4 * G], lam=scal[4 * G], h_hat=scal[4 * G + 1],
+                T=scal[4 * G + 2], n=scal[4 * G + 3])
+
+
+def topb_band_ok(idx_gpu, s_or, B):
+    """Symmetric difference limited to the tolerance band at the cut."""
+    I_or = O.topb_select(s_or, B)
+    diff = np.setxor1d(np.asarray(idx_gpu, np.int64), I_or)
+    if diff.size == 0:
+        return True, 0
+    sB = np.sort(s_or)[::-1][B - 1]
+    ok = np.all(np.abs(s_or[diff] - sB) <= REL * sB)
+    return bool(ok), int(diff.size)
+
+
+def check_layer(tag, K, V, L, W, spans, F, B, op: O.Params, G, gpu: dict,
+                orc: dict, report: dict):
+    """Compare one layer.  K, V: storage arrays [G, L, d]; gpu: this layer's
+    GPU outputs; orc: the oracle's compress_layer output (end to end)."""
+    Lp = L - W
+    f = scal_fields(gpu["scal"], G)
+    S_g = gpu["S"].astype(np.float64)
+    sbar_g = gpu["sbar"].astype(np.float64)
+    gst_g = gpu["gstar"].astype(np.int64)
+    s_g = gpu["s"].astype(np.float64)
+    idx_g = gpu["idx"].astype(np.int64)
+
+    # ---- scoring, end to end
+    r_S = max_rel(S_g, orc["S"])
+    r_sbar = max_rel(sbar_g, orc["sbar"])
+    assert r_S <= REL, f"{tag}: S rel err {r_S}"
+    assert r_sbar <= REL, f"{tag}: sbar rel err {r_sbar}"
+    mism = np.nonzero(gst_g != orc["gstar"])[0]
+    if mism.size:
+        So = orc["S"]
+        a = So[gst_g[mism], mism]
+        b = So[orc["gstar"][mism], mism]
+        assert np.all(np.abs(a - b) <= 1e-5 * b), f"{tag}: g* differs off a tie"
+        assert mism.size <= max(1, Lp // 1000), f"{tag}: {mism.size} g* near-ties"
+
+    # ---- MI prior, stage-wise on the GPU's S (identical float32 values)
+    is_vis, frame, r, c, rows, cols = O.visual_metadata(spans, Lp)
+    vis = np.nonzero(is_vis)[0]
+    cells = O.spatial_cells(r[vis], c[vis], rows[vis], cols[vis], op.grid)
+    mi_stage = np.array([O.plugin_mi(O.rank_bins(S_g[g, vis], op.n_bins), cells,
+                                     op.n_bins, op.grid * op.grid) for g in range(G)])
+    assert np.max(np.abs(f["mi"] - mi_stage)) <= 1e-5, f"{tag}: MI stage {f['mi']} vs {mi_stage}"
+    w_stage = O.mi_prior(f["mi_bar"].astype(np.float64), op.tau, op.eps)
+    assert np.max(np.abs(f["w"] - w_stage)) <= 1e-5, f"{tag}: w stage"
+    h_stage, T_stage = O.entropy_temperature(sbar_g, op.t_min, op.t_max, op.eps)
+    assert abs(f["h_hat"] - h_stage) <= 1e-5 and abs(f["T"] - T_stage) <= 1e-5, f"{tag}: H/T stage"
+
+    # ---- online statistics, end to end
+    assert np.max(np.abs(f["mi"] - orc["mi"])) <= 2e-3, f"{tag}: MI e2e {f['mi']} vs {orc['mi']}"
+    assert np.max(np.abs(f["mi_bar"] - orc["mi_bar"])) <= 2e-3, f"{tag}: MI_bar e2e"
+    assert abs(f["lam"] - orc["lam_eff"]) <= 1e-6, f"{tag}: lambda"
+    assert np.max(np.abs(f["phi"] - orc["phi"])) <= 1e-4, f"{tag}: phi {f['phi']} vs {orc['phi']}"
+    assert abs(f["h_hat"] - orc["h_hat"]) <= 1e-4 and abs(f["T"] - orc["T"]) <= 1e-4, f"{tag}: H/T"
+
+    # ---- fused score, stage-wise from the GPU's scalars
+    lam = float(f["lam"])
+    beta = (1.0 - lam) + lam * G * f["w"].astype(np.float64)[gst_g]
+    D = O.temporal_discount(is_vis, frame, F, f["phi"].astype(np.float64)[gst_g],
+                            op.delta, op.d_min)
+    _, s_stage = O.final_score(sbar_g, beta, D, float(f["T"]))
+    r_s_stage = max_rel(s_g, s_stage)
+    assert r_s_stage <= 1e-4, f"{tag}: s stage rel {r_s_stage}"
+    r_s = max_rel(s_g, orc["s"])
+    assert r_s <= REL, f"{tag}: s e2e rel {r_s}"
+
+    # ---- selection: exact on the GPU's own float32 scores; band vs oracle
+    assert idx_g.shape == (B,)
+    if B:
+        assert np.all(np.diff(idx_g) > 0), f"{tag}: idx not ascending"
+        s32 = gpu["s"]
+        order = np.lexsort((np.arange(Lp), -s32.astype(np.float64)))
+        want = np.sort(order[:B])
+        assert np.array_equal(idx_g, want), f"{tag}: idx != top-B of the GPU scores"
+    ok, ndiff = topb_band_ok(idx_g, orc["s"], B) if B else (True, 0)
+    assert ok, f"{tag}: idx differs from the oracle outside the tolerance band"
+
+    # ---- gather: bit-exact rows
+    Ko, Vo = O.gather_compact(K, V, idx_g, L, W)
+    assert np.array_equal(gpu["k_out"], Ko), f"{tag}: K' not bit-exact"
+    assert np.array_equal(gpu["v_out"], Vo), f"{tag}: V' not bit-exact"
+    if ndiff == 0:
+        assert np.array_equal(gpu["k_out"], orc["K_out"])
+
+    report.setdefault("S", []).append(r_S)
+    report.setdefault("s", []).append(r_s)
+    report.setdefault("idx_band", []).append(ndiff)
+    report.setdefault("gstar_ties", []).append(int(mism.size))

@@ -1,0 +1,216 @@
+"""GPU parity: the HIP path through the C ABI against the fp64 CPU oracle.
+
+Each case prints its name before touching the GPU.  The comparison bar is
+stated in tests/parity.py.
+"""
+
+import numpy as np
+import pytest
+
+torch = pytest.importorskip("torch")
+
+from oracle import starkv_oracle as O  # noqa: E402
+from paper_2606_01790_amd import starkv as sk  # noqa: E402
+from paper_2606_01790_amd import workload as WL  # noqa: E402
+from paper_2606_01790_amd.pipeline import ArrayCase, TrajectoryRunner  # noqa: E402
+from parity import check_layer, oracle_params  # noqa: E402
+
+pytestmark = pytest.mark.gpu
+
+
+def say(msg):
+    print(f"[parity] {msg}", flush=True)
+
+
+def params_for(cid, prior_active=False):
+    p = sk.params_default()
+    if cid >= 3:                    # multi-step (AgentNetBench-style) T range
+        p.t_min, p.t_max = 0.95, 1.05
+    if prior_active:                # lambda_eff = lambda from the first step
+        p.n_warmup, p.n_ramp = 0, 0
+    return p
+
+
+class HostFrames:
+    """Host copies of a trajectory's inputs, straight from the generator."""
+
+    def __init__(self, spec):
+        self.spec = spec
+        self.tr = WL.Trajectory(spec)
+        self.frames = {}
+
+    def cache(self, layer, step):
+        ks, vs = [], []
+        for f in range(1, step + 1):
+            if (layer, f) not in self.frames:
+                self.frames[(layer, f)] = self.tr.frame_kv(layer, f)
+            k, v = self.frames[(layer, f)]
+            ks.append(k)
+            vs.append(v)
+        k, v = self.tr.text_kv(layer, step)
+        return np.concatenate(ks + [k], axis=1), np.concatenate(vs + [v], axis=1)
+
+
+def run_trajectory(cid, layers=None, prior_active=False, steps=None):
+    spec = WL.SPECS[cid]
+    p = params_for(cid, prior_active)
+    op = oracle_params(p)
+    say(f"cfg{cid} prior_active={prior_active}: allocate")
+    runner = TrajectoryRunner(spec, p)
+    runner.reset()
+    host = HostFrames(spec)
+    layers = list(range(spec.n_layers)) if layers is None else list(layers)
+    states = {l: O.LayerState(spec.G) for l in layers}
+    report = {}
+    for step in range(1, (steps or spec.steps) + 1):
+        say(f"cfg{cid} step {step}: load + score/update")
+        runner.load_step(step)
+        runner.score_and_update(step)
+        L, W = spec.L(step), spec.W
+        spans = spec.spans(step)
+        budgets = spec.budgets(step)
+        orc_base = {}
+        for layer in layers:
+            K, V = host.cache(layer, step)
+            Q = host.tr.window_q(layer, step)
+            out, states[layer] = O.compress_layer(
+                WL.to_float64(Q, spec.dtype), WL.to_float64(K, spec.dtype), None, L, W,
+                spans, step, budgets[0], op, states[layer], copy_rows=(K, V))
+            orc_base[layer] = (out, K, V)
+        for B in budgets:
+            say(f"cfg{cid} step {step} B={B}: select/compact")
+            runner.select_and_compact(step, B)
+            torch.cuda.synchronize()
+            gpu = runner.outputs(step, B)
+            for layer in layers:
+                out, K, V = orc_base[layer]
+                orc = dict(out)
+                orc["I"] = O.topb_select(out["s"], B)
+                orc["K_out"], orc["V_out"] = O.gather_compact(K, V, orc["I"], L, W)
+                g = {k: v[layer] for k, v in gpu.items()}
+                check_layer(f"cfg{cid} step{step} L{layer} B{B}", K, V, L, W, spans,
+                            step, B, op, spec.G, g, orc, report)
+    say(f"cfg{cid} done: max S rel {max(report['S']):.2e}, max s rel "
+        f"{max(report['s']):.2e}, idx band tokens {sum(report['idx_band'])}, "
+        f"g* near-ties {sum(report['gstar_ties'])}")
+    return report
+
+
+def test_config1_tiny_f32():
+    run_trajectory(1)
+
+
+def test_config2_single_layer_bf16():
+    run_trajectory(2)
+
+
+def test_config2_prior_active():
+    run_trajectory(2, prior_active=True)
+
+
+def test_config3_28_layers_5_steps():
+    run_trajectory(3)
+
+
+def test_config3_prior_active_sampled_layers():
+    run_trajectory(3, layers=[0, 1, 2, 3, 27], prior_active=True)
+
+
+def test_config4_budget_sweep_sampled_layers():
+    """15 steps, three budgets per step; the oracle follows layers 0 and 13
+    through the whole trajectory (their state depends on every step)."""
+    run_trajectory(4, layers=[0, 13])
+
+
+def test_determinism_bitwise():
+    spec = WL.SPECS[2]
+    p = params_for(2, prior_active=True)
+    outs = []
+    for rep in range(2):
+        say(f"determinism run {rep}")
+        r = TrajectoryRunner(spec, p)
+        r.reset()
+        r.load_step(1)
+        r.run_step(1, spec.budgets(1)[0])
+        torch.cuda.synchronize()
+        outs.append(r.outputs(1, spec.budgets(1)[0]))
+    for k in outs[0]:
+        assert np.array_equal(outs[0][k], outs[1][k]), k
+
+
+# ------------------------------------------------------------------ edge cases
+
+def run_case(tag, H, G, d, W, L, spans, F, B, dtype, p, seed=0, n_layers=2,
+             L_cap=None, Qs=None, Ks=None, Vs=None, case=None, states=None):
+    L_cap = L_cap or L
+    if Qs is None:
+        Qs, Ks, Vs = WL.random_case(seed, n_layers, H, G, d, L_cap, W, dtype)
+    frame_cap = max([r * c for (_, r, c, _) in spans] + [1])
+    case = case or ArrayCase(H, G, d, W, n_layers, L_cap, dtype, p, frame_cap)
+    say(f"{tag}: H={H} G={G} d={d} W={W} L={L} B={B} {dtype}")
+    gpu = case.run(Qs, Ks, Vs, L, spans, F, B)
+    op = oracle_params(p)
+    states = states if states is not None else [O.LayerState(G) for _ in range(n_layers)]
+    report = {}
+    for layer in range(n_layers):
+        K = Ks[layer][:, :L]
+        V = Vs[layer][:, :L]
+        out, states[layer] = O.compress_layer(
+            WL.to_float64(Qs[layer], dtype), WL.to_float64(K, dtype), None, L, W, spans,
+            F, B, op, states[layer], copy_rows=(K, V))
+        g = {k: v[layer] for k, v in gpu.items()}
+        check_layer(f"{tag} L{layer}", K, V, L, W, spans, F, B, op, G, g, out, report)
+    return case, states
+
+
+def test_ragged_rows_and_tokens_bf16():
+    """R = 5*7 = 35 window rows (a padded MFMA block), L_p = 1000 (a ragged
+    token tail), spans at odd offsets with text between them."""
+    p = params_for(3, prior_active=True)
+    spans = [(3, 7, 11, 1), (100, 13, 9, 2), (300, 20, 30, 3)]
+    run_case("ragged", 28, 4, 128, 5, 1005, spans, 3, 137, "bf16", p, seed=1)
+
+
+def test_budget_extremes():
+    p = params_for(2)
+    spans = [(0, 10, 20, 1)]
+    for B in (0, 1, 400 - 8):
+        run_case(f"B={B}", 8, 2, 64, 8, 400, spans, 1, B, "bf16", p, seed=2)
+
+
+def test_mha_f32_d128_and_strided_cache():
+    """G = H (per-head subspaces) in fp32 with d = 128, cache capacity above L."""
+    p = params_for(2)
+    spans = [(0, 12, 16, 1)]
+    run_case("mha", 4, 4, 128, 4, 250, spans, 1, 40, "f32", p, seed=3, L_cap=333)
+
+
+def test_exact_ties_everywhere():
+    """All keys zero: uniform attention, so scores tie exactly in the interior.
+    Rank bins and the top-B cut must then follow token order on both sides."""
+    p = params_for(2, prior_active=True)
+    H, G, d, W, L = 8, 2, 128, 8, 600
+    Qs, Ks, Vs = WL.random_case(4, 2, H, G, d, L, W, "bf16")
+    Ks = np.zeros_like(Ks)
+    spans = [(10, 20, 25, 1)]
+    run_case("ties", H, G, d, W, L, spans, 1, 50, "bf16", p, Qs=Qs, Ks=Ks, Vs=Vs)
+
+
+def test_frame_size_change_resets_stability():
+    """Two steps whose current frames differ in size: m_g restarts, phi = 0."""
+    p = params_for(3, prior_active=True)
+    H, G, d, W = 8, 2, 64, 8
+    L1, L2 = 300, 500
+    case = None
+    states = None
+    seq = [(L1, [(0, 10, 20, 1)], 1),
+           (L2, [(0, 10, 20, 1), (250, 12, 15, 2)], 2),
+           (L2, [(0, 10, 20, 1), (250, 12, 15, 2)], 2)]
+    for step, (L, spans, F) in enumerate(seq, 1):
+        Qs, Ks, Vs = WL.random_case(10 + step, 2, H, G, d, L, W, "bf16")
+        if case is None:
+            case = ArrayCase(H, G, d, W, 2, L2, "bf16", p, 200)
+        case, states = run_case(f"resize step{step}", H, G, d, W, L, spans, F, 60,
+                                "bf16", p, n_layers=2, Qs=Qs, Ks=Ks, Vs=Vs, case=case,
+                                states=states)
+    assert states[0].m.shape == (2, 180)
