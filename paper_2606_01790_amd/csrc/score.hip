@@ -62,6 +62,13 @@ __device__ inline const T* group_k(const ScoreArgs& a, int layer, int g) {
   return reinterpret_cast<const T*>(a.k) + (int64_t)layer * a.ls + (int64_t)g * a.gs;
 }
 
+// 2^((m - mn) * scale) for a running max m <= mn, ms = mn * scale.  Exactly 1
+// when the max did not move: with the -1e30 start value the fma would
+// otherwise return the rounding residual of the product, not 0.
+__device__ inline float rescale(float m, float mn, float ms, float scale) {
+  return m == mn ? 1.0f : __builtin_amdgcn_exp2f(fmaf(m, scale, -ms));
+}
+
 // ---------------------------------------------------------------- pass 1
 template <typename T, int D, int NRBM>
 __global__ __launch_bounds__(256) void score_pass1(ScoreArgs a) {
@@ -114,7 +121,7 @@ __global__ __launch_bounds__(256) void score_pass1(ScoreArgs a) {
         float sum = 0.f;
 #pragma unroll
         for (int e = 0; e < 16; ++e) sum += __builtin_amdgcn_exp2f(fmaf(acc[e], a.scale, -ms));
-        l[rb] = l[rb] * __builtin_amdgcn_exp2f(fmaf(m[rb], a.scale, -ms)) + sum;
+        l[rb] = l[rb] * rescale(m[rb], mn, ms, a.scale) + sum;
         m[rb] = mn;
       }
     }
@@ -126,8 +133,7 @@ __global__ __launch_bounds__(256) void score_pass1(ScoreArgs a) {
       const float mo = __shfl_xor(m[rb], 32), lo = __shfl_xor(l[rb], 32);
       const float mn = fmaxf(m[rb], mo);
       const float ms = mn * a.scale;
-      l[rb] = l[rb] * __builtin_amdgcn_exp2f(fmaf(m[rb], a.scale, -ms)) +
-              lo * __builtin_amdgcn_exp2f(fmaf(mo, a.scale, -ms));
+      l[rb] = l[rb] * rescale(m[rb], mn, ms, a.scale) + lo * rescale(mo, mn, ms, a.scale);
       m[rb] = mn;
       if (half == 0) red[wave * a.Rpad + rb * 32 + l32] = make_float2(mn * a.scale, l[rb]);
     }
@@ -169,7 +175,7 @@ __global__ __launch_bounds__(256) void score_pass2(ScoreArgs a) {
       lx = lx * __builtin_amdgcn_exp2f(Mx - mn) + p.y * __builtin_amdgcn_exp2f(p.x - mn);
       Mx = mn;
     }
-    cst[r] = (r < a.R) ? Mx + __log2f(lx) : INFINITY;
+    cst[r] = (r < a.R) ? Mx + log2f(lx) : INFINITY;
   }
   __syncthreads();
 

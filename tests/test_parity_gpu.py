@@ -171,6 +171,19 @@ def test_ragged_rows_and_tokens_bf16():
     run_case("ragged", 28, 4, 128, 5, 1005, spans, 3, 137, "bf16", p, seed=1)
 
 
+@pytest.mark.parametrize("Lp", [1, 31, 33, 257, 260, 288, 292, 319, 511, 513, 1100])
+def test_token_tail_sweep(Lp):
+    """Past-token counts around the 32-token MFMA blocks and the 256-token
+    chunks: waves and lane halves that see only masked tokens."""
+    p = params_for(2)
+    W = 8
+    L = Lp + W
+    n = min(Lp, 12) * min(max(Lp // 12, 1), 10)
+    spans = [(0, min(Lp, 12), min(max(Lp // 12, 1), 10), 1)] if n <= Lp else []
+    run_case(f"tail Lp={Lp}", 8, 2, 64, W, L, spans, 1, max(Lp // 5, 1), "bf16", p,
+             seed=Lp)
+
+
 def test_budget_extremes():
     p = params_for(2)
     spans = [(0, 10, 20, 1)]
