@@ -1,0 +1,356 @@
+#!/usr/bin/env python3
+"""Throughput of the STaR-KV compression stage on one MI355X.
+
+One bench step is one whole pass of the hot path over the workload: every
+trajectory step of the 28-layer, 5-screenshot trajectory (Qwen2.5-VL-7B
+GQA shape, bf16), each running starkv_score, starkv_update_state,
+starkv_select and starkv_compact for all layers.  The caches of every
+trajectory step, the window queries and a fresh per-trajectory state are
+resident in HBM before the timed region starts.
+
+Prints one JSON line:
+  value      compressed visual tokens per second per layer: the sum over
+             trajectory steps and layers of N_vis, divided by the time;
+  roofline   the dominant call's achieved algorithmic bandwidth against the
+             8 TB/s HBM peak, from HIP events on its stream;
+  cpu_baseline  the fp64 CPU oracle on a bounded sample of the same work.
+"""
+
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0
+METRIC = "compressed visual KV tokens/s per layer (score+select+gather); % HBM peak"
+
+
+def parse():
+    ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=30)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--config", type=int, default=3)
+    ap.add_argument("--cpu-layers", type=int, default=6,
+                    help="layers in the oracle's timed sample (all trajectory steps)")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--eager", action="store_true",
+                    help="launch every call from Python instead of replaying a HIP graph")
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help="also run one plain 1 GiB device copy (counter calibration)")
+    return ap.parse_args()
+
+
+def log(msg):
+    print(f"[bench] {msg}", file=sys.stderr, flush=True)
+
+
+class Workload:
+    """Resident inputs and outputs of one trajectory of `spec`."""
+
+    def __init__(self, spec, params, n_states, device="cuda"):
+        import torch
+        from paper_2606_01790_amd import starkv as sk
+        from paper_2606_01790_amd.pipeline import to_device
+        from paper_2606_01790_amd.workload import Trajectory
+
+        self.spec, self.params, self.sk = spec, params, sk
+        sp = spec
+        dt = torch.bfloat16 if sp.dtype == "bf16" else torch.float32
+        self.dt = sk.BF16 if sp.dtype == "bf16" else sk.F32
+        tr = Trajectory(sp)
+        nl, G, H, d, W, nf = sp.n_layers, sp.G, sp.H, sp.d, sp.W, sp.n_frame
+        frames_k = torch.empty((sp.steps, nl, G, nf, d), dtype=dt, device=device)
+        frames_v = torch.empty_like(frames_k)
+        for f in range(1, sp.steps + 1):
+            for layer in range(nl):
+                k, v = tr.frame_kv(layer, f)
+                frames_k[f - 1, layer] = to_device(k, sp.dtype, device)
+                frames_v[f - 1, layer] = to_device(v, sp.dtype, device)
+        self.K, self.V, self.Q, self.layout = [], [], [], []
+        for s in range(1, sp.steps + 1):
+            tk = torch.empty((nl, G, sp.text, d), dtype=dt, device=device)
+            tv = torch.empty_like(tk)
+            q = torch.empty((nl, H, W, d), dtype=dt, device=device)
+            for layer in range(nl):
+                k, v = tr.text_kv(layer, s)
+                tk[layer] = to_device(k, sp.dtype, device)
+                tv[layer] = to_device(v, sp.dtype, device)
+                q[layer] = to_device(tr.window_q(layer, s), sp.dtype, device)
+            K = torch.cat([frames_k[f] for f in range(s)] + [tk], dim=2).contiguous()
+            V = torch.cat([frames_v[f] for f in range(s)] + [tv], dim=2).contiguous()
+            self.K.append(K)
+            self.V.append(V)
+            self.Q.append(q)
+            self.layout.append(sk.contiguous_layout(K, self.dims(s)))
+        del frames_k, frames_v
+        Lp, B = sp.L_p(sp.steps), max(max(sp.budgets(s)) for s in range(1, sp.steps + 1))
+        f32 = torch.float32
+        self.S = torch.empty(nl * G * Lp, dtype=f32, device=device)
+        self.sbar = torch.empty(nl * Lp, dtype=f32, device=device)
+        self.gstar = torch.empty(nl * Lp, dtype=torch.uint8, device=device)
+        self.s = torch.empty(nl * Lp, dtype=f32, device=device)
+        self.idx = torch.empty(nl * B, dtype=torch.int32, device=device)
+        self.k_out = torch.empty(nl * G * (B + W) * d, dtype=dt, device=device)
+        self.v_out = torch.empty_like(self.k_out)
+        dmax = self.dims(sp.steps)
+        self.ws = torch.empty(sk.workspace_bytes(dmax), dtype=torch.uint8, device=device)
+        self.nscal = sk.scalars_count(dmax)
+        self.scal = torch.empty(nl * self.nscal, dtype=f32, device=device)
+        self.frame_cap = nf
+        self.states = [torch.empty(sk.state_bytes(dmax, nf), dtype=torch.uint8,
+                                   device=device) for _ in range(n_states)]
+        for st in self.states:
+            sk.state_init(dmax, st, nf)
+        torch.cuda.synchronize()
+
+    def dims(self, s):
+        sp = self.spec
+        return self.sk.make_dims(sp.n_layers, sp.H, sp.G, sp.d, sp.L(s), sp.W, self.dt)
+
+    def trajectory(self, state):
+        """The hot path over the whole trajectory: the four calls per step."""
+        sk, sp, p = self.sk, self.spec, self.params
+        for s in range(1, sp.steps + 1):
+            i = s - 1
+            dims = self.dims(s)
+            spans = sp.spans(s)
+            B = sp.budgets(s)[0]
+            sk.score(dims, p, self.Q[i], self.K[i], self.layout[i], self.S, self.sbar,
+                     self.gstar, self.ws)
+            sk.update_state(dims, p, self.S, self.sbar, spans, s, state, self.frame_cap,
+                            self.scal, self.ws)
+            sk.select(dims, p, self.sbar, self.gstar, self.scal, spans, s, B, self.s,
+                      self.idx, self.ws)
+            sk.compact(dims, self.K[i], self.V[i], self.layout[i], self.idx, B, self.k_out,
+                       self.v_out)
+
+
+def call_bytes(spec, s, name):
+    """Algorithmic HBM bytes of one call at trajectory step s, all layers:
+    inputs read once and outputs written once."""
+    sp = spec
+    e, nl, H, G, d, W = sp.elem_bytes, sp.n_layers, sp.H, sp.G, sp.d, sp.W
+    Lp, nv, nf, B = sp.L_p(s), sp.n_vis(s), sp.n_frame, sp.budgets(s)[0]
+    if name == "score":        # Q, K_past in; S, sbar, g* out
+        per = e * (H * W * d + G * Lp * d) + 4 * G * Lp + 4 * Lp + Lp
+    elif name == "update_state":   # S of visual tokens, sbar, stability means
+        per = 4 * G * nv + 4 * Lp + 4 * G * nf * 3
+    elif name == "select":     # sbar, g* in; s, idx out
+        per = 5 * Lp + 4 * Lp + 4 * B
+    else:                      # idx in; B+W rows of K and V in and out
+        per = 4 * B + 4 * G * (B + W) * d * e
+    return nl * per
+
+
+def per_call_timing(wl, spec, sk, torch, reps):
+    """Average GPU time of each call, per trajectory step: `reps` launches of
+    the call back to back, captured in a HIP graph and timed with HIP events
+    on the replay stream.  update_state runs on a scratch state."""
+    p = wl.params
+    scratch = wl.states[-2]
+    per = {}
+    stream = torch.cuda.current_stream()
+    for s in range(1, spec.steps + 1):
+        i = s - 1
+        dims, spans, B = wl.dims(s), spec.spans(s), spec.budgets(s)[0]
+        calls = {
+            "score": lambda: sk.score(dims, p, wl.Q[i], wl.K[i], wl.layout[i], wl.S,
+                                      wl.sbar, wl.gstar, wl.ws),
+            "update_state": lambda: sk.update_state(dims, p, wl.S, wl.sbar, spans, s,
+                                                    scratch, wl.frame_cap, wl.scal, wl.ws),
+            "select": lambda: sk.select(dims, p, wl.sbar, wl.gstar, wl.scal, spans, s, B,
+                                        wl.s, wl.idx, wl.ws),
+            "compact": lambda: sk.compact(dims, wl.K[i], wl.V[i], wl.layout[i], wl.idx, B,
+                                          wl.k_out, wl.v_out),
+        }
+        for name, fn in calls.items():
+            g = torch.cuda.CUDAGraph()
+            with torch.cuda.graph(g):
+                for _ in range(reps):
+                    fn()
+            g.replay()
+            torch.cuda.synchronize()
+            e0 = torch.cuda.Event(enable_timing=True)
+            e1 = torch.cuda.Event(enable_timing=True)
+            e0.record(stream)
+            g.replay()
+            e1.record(stream)
+            torch.cuda.synchronize()
+            d = per.setdefault(name, {"time": 0.0, "launches": 0, "bytes": 0})
+            d["time"] += e0.elapsed_time(e1) * 1e-3
+            d["launches"] += reps
+            d["bytes"] += reps * call_bytes(spec, s, name)
+    return per
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print("bench.py: this build runs the compression stage on one GPU only; "
+              "a multi-GPU run is not supported (use --gpus 1).", file=sys.stderr)
+        sys.exit(2)
+    import numpy as np
+    import torch
+
+    from paper_2606_01790_amd import starkv as sk
+    from paper_2606_01790_amd import workload as WL
+
+    assert torch.cuda.is_available(), "no GPU visible"
+    spec = WL.SPECS[args.config]
+    params = sk.params_default()
+    if args.config >= 3:
+        params.t_min, params.t_max = 0.95, 1.05
+    log(f"workload {spec.name}: building resident inputs")
+    n_states = args.warmup + 3
+    wl = Workload(spec, params, n_states)
+    layer_tokens = spec.n_layers * sum(spec.n_vis(s) for s in range(1, spec.steps + 1))
+    bytes_alg = spec.n_layers * sum(WL.bytes_alg(spec, s, spec.budgets(s)[0])
+                                    for s in range(1, spec.steps + 1))
+
+    log(f"warmup {args.warmup}")
+    k = 0
+    for _ in range(args.warmup):
+        wl.trajectory(wl.states[k])
+        k += 1
+    torch.cuda.synchronize()
+
+    stream = torch.cuda.current_stream()
+    if args.eager:
+        run = lambda: wl.trajectory(wl.states[0])  # noqa: E731
+    else:
+        # One trajectory (a fresh state, then every step's four calls) captured
+        # into a HIP graph: the timed region replays it, so the host's Python
+        # launch cost does not starve the GPU.
+        graph_state = wl.states[-1]
+        dmax = wl.dims(spec.steps)
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g):
+            sk.state_init(dmax, graph_state, wl.frame_cap)
+            wl.trajectory(graph_state)
+        torch.cuda.synchronize()
+        run = g.replay
+        for _ in range(args.warmup):
+            run()
+        torch.cuda.synchronize()
+
+    log(f"timed {args.steps} steps ({'eager' if args.eager else 'graph replay'})")
+    e0 = torch.cuda.Event(enable_timing=True)
+    e1 = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    e0.record(stream)
+    for _ in range(args.steps):
+        run()
+    e1.record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    gpu_ms = e0.elapsed_time(e1)
+    ms_per_step = max(gpu_ms, wall * 1e3) / args.steps
+    value = layer_tokens / (ms_per_step * 1e-3)
+
+    log("per-call timing: graphs of back-to-back launches of one call")
+    per = per_call_timing(wl, spec, sk, torch, reps=10)
+    dom = max(per, key=lambda n: per[n]["time"])
+    dd = per[dom]
+    avg_s = dd["time"] / dd["launches"]
+    avg_b = dd["bytes"] / dd["launches"]
+    achieved = avg_b / avg_s / 1e9
+    roofline = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS,
+                "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
+                "traffic": None, "kernel": f"starkv_{dom}",
+                "avg_launch_us": round(avg_s * 1e6, 2),
+                "alg_bytes_per_launch": int(avg_b)}
+    per_call_us = {n: round(per[n]["time"] / per[n]["launches"] * 1e6, 2) for n in per}
+
+    cpu = None
+    if not args.no_cpu_baseline:
+        cpu = cpu_baseline(spec, params, args.cpu_layers)
+
+    line = {
+        "metric": METRIC,
+        "value": round(value, 1),
+        "unit": "layer-tokens/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": spec.dtype,
+        "data": "synthetic",
+        "config": {"workload": spec.name, "n_layers": spec.n_layers, "H": spec.H,
+                   "G": spec.G, "d": spec.d, "W": spec.W,
+                   "trajectory_steps": spec.steps, "budget_pct": list(spec.pcts),
+                   "layer_tokens_per_step": layer_tokens,
+                   "bytes_alg_per_step": bytes_alg,
+                   "launch": "eager" if args.eager else "hipgraph"},
+        "hbm_frac_path": round(bytes_alg / (ms_per_step * 1e-3) / (HBM_PEAK_GBS * 1e9), 4),
+        "per_call_us": per_call_us,
+        "roofline": roofline,
+        "cpu_baseline": cpu,
+    }
+    if args.copy_calibration:
+        n = 1 << 30
+        a = torch.empty(n, dtype=torch.uint8, device="cuda")
+        b = torch.empty_like(a)
+        b.copy_(a)
+        torch.cuda.synchronize()
+        line["copy_calibration_bytes"] = n
+    print(json.dumps(line), flush=True)
+
+
+def cpu_baseline(spec, params, n_layers_sample):
+    """The fp64 oracle, untuned, on the host: every trajectory step of the
+    first `n_layers_sample` layers (a layer-tokens/s rate, like the metric)."""
+    import numpy as np
+    from oracle import starkv_oracle as O
+    from paper_2606_01790_amd import workload as WL
+
+    try:
+        from threadpoolctl import threadpool_info
+        blas = [i.get("num_threads", 1) for i in threadpool_info()
+                if i.get("user_api") == "blas"]
+        threads = max(blas) if blas else 1
+    except Exception:
+        threads = 1
+    op = O.Params(lam=params.lam, n_warmup=params.n_warmup, n_ramp=params.n_ramp,
+                  rho_mi=params.rho_mi, tau=params.tau, rho_t=params.rho_t,
+                  delta=params.delta, d_min=params.d_min, t_min=params.t_min,
+                  t_max=params.t_max, n_bins=params.n_bins, grid=params.grid,
+                  pool_kernel=params.pool_kernel, eps=params.eps)
+    tr = WL.Trajectory(spec)
+    nl = min(n_layers_sample, spec.n_layers)
+    inputs = []
+    for layer in range(nl):
+        for s in range(1, spec.steps + 1):
+            K, V = tr.layer_cache(layer, s)
+            inputs.append((layer, s, WL.to_float64(tr.window_q(layer, s), spec.dtype),
+                           WL.to_float64(K, spec.dtype), K, V))
+    states = {l: O.LayerState(spec.G) for l in range(nl)}
+    log(f"cpu baseline: oracle on {nl} layers x {spec.steps} steps")
+    t0 = time.perf_counter()
+    tokens = 0
+    for layer, s, Q, K64, K, V in inputs:
+        _, states[layer] = O.compress_layer(Q, K64, None, spec.L(s), spec.W, spec.spans(s),
+                                            s, spec.budgets(s)[0], op, states[layer],
+                                            copy_rows=(K, V))
+        tokens += spec.n_vis(s)
+    dt = time.perf_counter() - t0
+    return {"value": round(tokens / dt, 1), "unit": "layer-tokens/s", "cores": threads,
+            "kind": "oracle",
+            "sample": f"layers 0-{nl - 1}, all {spec.steps} trajectory steps "
+                      f"({tokens} layer-tokens, {dt:.1f} s, numpy fp64, BLAS threads "
+                      f"{threads})"}
+
+
+if __name__ == "__main__":
+    main()

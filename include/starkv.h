@@ -67,7 +67,8 @@ typedef enum starkv_dtype {
  * G KV groups, query head h reads group floor(h*G/H).  Requirements:
  * n_layers >= 1; G >= 1, G <= STARKV_MAX_GROUPS, H % G == 0; d in {64, 128};
  * 1 <= W < L; L <= 2^26; the window rows of one group, R = W*H/G, must
- * satisfy R <= 512 and R*(d*elem_bytes + 16) <= 128 KiB (R rounded up to 32). */
+ * satisfy R <= 512 and R*(d*elem_bytes + 16) <= 128 KiB (R rounded up to 32);
+ * for STARKV_F32, R <= 128. */
 typedef struct starkv_dims {
   int32_t n_layers;
   int32_t H;

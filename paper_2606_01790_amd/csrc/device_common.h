@@ -10,6 +10,7 @@ namespace starkv {
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef int i32x4 __attribute__((ext_vector_type(4)));
 
 constexpr int kWave = 64;
 
@@ -95,6 +96,81 @@ __device__ inline int block_excl_count(bool flag, int* sh, int* total) {
   }
   *total = tot;
   return before + in_wave;
+}
+
+
+// Inclusive prefix sum of an int across the 64 lanes of a wave.
+__device__ inline int wave_incl_scan(int v) {
+  const int lane = threadIdx.x & 63;
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) {
+    const int t = __shfl_up(v, o);
+    if (lane >= o) v += t;
+  }
+  return v;
+}
+
+__device__ inline uint32_t wave_min_u32(uint32_t v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v = min(v, (uint32_t)__shfl_xor((int)v, o));
+  return v;
+}
+
+__device__ inline uint32_t wave_max_u32(uint32_t v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v = max(v, (uint32_t)__shfl_xor((int)v, o));
+  return v;
+}
+
+// Exclusive prefix sum of an int over the block in thread order; all threads
+// get the block total.  `sh` holds blockDim.x / 64 ints.
+__device__ inline int block_excl_scan(int v, int* sh, int* total) {
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  const int nw = blockDim.x >> 6;
+  const int inc = wave_incl_scan(v);
+  __syncthreads();
+  if (lane == 63) sh[w] = inc;
+  __syncthreads();
+  int before = 0, tot = 0;
+  for (int i = 0; i < nw; ++i) {
+    const int c = sh[i];
+    if (i < w) before += c;
+    tot += c;
+  }
+  *total = tot;
+  return before + inc - v;
+}
+
+// One wave: in the histogram h[0..nb) (nb <= 256), the bin d whose running
+// count range [before, before + h[d]) contains `rank` (rank < sum of h).
+__device__ inline void wave_find_bin(const int* h, int nb, int rank, int* d_out,
+                                     int* before_out, int* cnt_out) {
+  const int lane = threadIdx.x & 63;
+  int c[4];
+#pragma unroll
+  for (int j = 0; j < 4; ++j) c[j] = (4 * lane + j < nb) ? h[4 * lane + j] : 0;
+  const int sum = c[0] + c[1] + c[2] + c[3];
+  const int inc = wave_incl_scan(sum);
+  const int exc = inc - sum;
+  const uint64_t hit = __ballot(exc <= rank && rank < inc);
+  const int src = hit ? __ffsll((unsigned long long)hit) - 1 : 0;
+  int d = 0, before = 0, cnt = 0;
+  if (lane == src) {
+    int run = exc;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      if (rank < run + c[j]) { d = 4 * lane + j; before = run; cnt = c[j]; break; }
+      run += c[j];
+    }
+  }
+  *d_out = __shfl(d, src);
+  *before_out = __shfl(before, src);
+  *cnt_out = __shfl(cnt, src);
+}
+
+// Bits [shift, 32) of a key, with shift = 32 giving 0.
+__device__ inline uint32_t key_hi(uint32_t k, int shift) {
+  return shift >= 32 ? 0u : (k >> shift);
 }
 
 }  // namespace starkv

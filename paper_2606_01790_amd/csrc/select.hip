@@ -2,11 +2,14 @@
 // sec. 3.7 selection).  One 1024-thread workgroup per layer:
 //   1. s_t = max(sbar_t * beta_t * D_t, 0)^(1/T) for every past token,
 //      written out and kept as a descending-order key in LDS;
-//   2. MSB-first radix select (8-bit digits) of the B-th key in the order
-//      (s descending, token index ascending);
-//   3. one ordered pass in token order flags the selected tokens (keys past
-//      the cut, plus the lowest-index ties at the cut) and compacts them with
-//      a block scan, so idx comes out ascending.
+//   2. MSB-first radix select of the B-th key in the order (s descending,
+//      token index ascending): the bits every key shares are skipped, then
+//      8-bit digits are counted in per-wave LDS histograms and the digit is
+//      found with a wave-wide prefix scan;
+//   3. ordered compaction: each wave owns a contiguous token segment, counts
+//      its selected tokens (keys past the cut, plus the lowest-index ties at
+//      the cut) with ballots, and writes them at its segment's offset, so idx
+//      comes out ascending.
 #include "device_common.h"
 #include "internal.h"
 
@@ -14,6 +17,8 @@ namespace starkv {
 namespace {
 
 constexpr int kThreads = 1024;
+constexpr int kWaves = kThreads / 64;
+constexpr int kBatch = 8;              // loads in flight per thread
 constexpr int kLdsKeys = 28 * 1024;   // keys cached in LDS (112 KiB)
 
 struct SelArgs {
@@ -43,13 +48,15 @@ __device__ inline int find_span(const SelArgs& a, int t) {
 
 __global__ __launch_bounds__(kThreads) void select_kernel(SelArgs a) {
   extern __shared__ __align__(16) uint32_t keys[];
-  __shared__ int hist[256];
+  __shared__ int hist[kWaves * 256];      // per-wave digit histograms
   __shared__ float w_s[STARKV_MAX_GROUPS], phi_s[STARKV_MAX_GROUPS];
+  __shared__ uint32_t red_lo[kWaves], red_hi[kWaves];
   __shared__ uint32_t cut_key;
   __shared__ int cut_rank, cut_eq;
-  __shared__ int sh_cnt[kThreads / 64];
+  __shared__ int wsel[kWaves], weq[kWaves];
 
   const int layer = blockIdx.x, tid = threadIdx.x;
+  const int lane = tid & 63, wave = tid >> 6;
   const float* scal = a.scal + (size_t)layer * a.sc;
   const float* sb = a.sbar + (size_t)layer * a.Lp;
   const uint8_t* gs = a.gstar + (size_t)layer * a.Lp;
@@ -64,81 +71,123 @@ __global__ __launch_bounds__(kThreads) void select_kernel(SelArgs a) {
   const float inv_t = 1.0f / T;
   const float gl = (float)a.G * lam;
 
-  // ---- 1. fused score
-  for (int t = tid; t < a.Lp; t += kThreads) {
-    const int g = min((int)gs[t], a.G - 1);
-    const float beta = (1.0f - lam) + gl * w_s[g];
-    float D = 1.0f;
-    const int sp = find_span(a, t);
-    if (sp >= 0) {
-      const float dist = (float)(a.frame - a.sframe[sp]);
-      D = a.d_min + (1.0f - a.d_min) * expf(-a.delta * dist * phi_s[g]);
+  // ---- 1. fused score; keys order tokens by descending s
+  uint32_t lo = 0xFFFFFFFFu, hi = 0u;
+  for (int t0 = tid; t0 < a.Lp; t0 += kBatch * kThreads) {
+    float sbv[kBatch];
+    int gv[kBatch];
+#pragma unroll
+    for (int u = 0; u < kBatch; ++u) {   // kBatch loads in flight
+      const int t = t0 + u * kThreads;
+      sbv[u] = t < a.Lp ? sb[t] : 0.f;
+      gv[u] = t < a.Lp ? (int)gs[t] : 0;
     }
-    const float sf = fmaxf(sb[t] * beta * D, 0.0f);
-    const float sv = (inv_t == 1.0f || sf == 0.0f) ? sf : exp2f(inv_t * log2f(sf));
-    s_out[t] = sv;
-    if (t < a.cache) keys[t] = ~fkey(sv);
+#pragma unroll
+    for (int u = 0; u < kBatch; ++u) {
+      const int t = t0 + u * kThreads;
+      if (t < a.Lp) {
+        const int g = min(gv[u], a.G - 1);
+        const float beta = (1.0f - lam) + gl * w_s[g];
+        float D = 1.0f;
+        const int sp = find_span(a, t);
+        if (sp >= 0) {
+          const float dist = (float)(a.frame - a.sframe[sp]);
+          D = a.d_min + (1.0f - a.d_min) * __expf(-a.delta * dist * phi_s[g]);
+        }
+        const float sf = fmaxf(sbv[u] * beta * D, 0.0f);
+        const float sv = (inv_t == 1.0f || sf == 0.0f) ? sf : exp2f(inv_t * __log2f(sf));
+        s_out[t] = sv;
+        const uint32_t k = ~fkey(sv);
+        if (t < a.cache) keys[t] = k;
+        lo = min(lo, k);
+        hi = max(hi, k);
+      }
+    }
   }
   if (a.B == 0) return;
+  lo = wave_min_u32(lo);
+  hi = wave_max_u32(hi);
+  if (lane == 0) { red_lo[wave] = lo; red_hi[wave] = hi; }
   __syncthreads();
+  uint32_t kmin = 0xFFFFFFFFu, kmax = 0u;
+  for (int w = 0; w < kWaves; ++w) { kmin = min(kmin, red_lo[w]); kmax = max(kmax, red_hi[w]); }
 
-  // ---- 2. radix select of rank B-1 in ascending ~key (= descending s)
-  if (tid == 0) {
-    cut_key = 0u;
-    cut_rank = a.B - 1;
-  }
-  for (int pass = 0; pass < 4; ++pass) {
-    const int shift = 24 - 8 * pass;
-    if (tid < 256) hist[tid] = 0;
+  // ---- 2. radix select of rank B-1, skipping the bits all keys share
+  const int common = (kmin == kmax) ? 32 : __clz(kmin ^ kmax);
+  const uint32_t cmask = common == 0 ? 0u : (common >= 32 ? 0xFFFFFFFFu : (0xFFFFFFFFu << (32 - common)));
+  uint32_t ck = kmin & cmask;
+  int crank = a.B - 1, ceq = a.Lp;
+  for (int done = common; done < 32;) {
+    const int width = min(8, 32 - done);
+    const int shift = 32 - done - width;
+    const int nb = 1 << width;
+    for (int i = tid; i < kWaves * 256; i += kThreads) hist[i] = 0;
     __syncthreads();
-    const uint32_t hi_want = pass == 0 ? 0u : (cut_key >> (shift + 8));
+    const uint32_t want = key_hi(ck, shift + width);
     for (int t = tid; t < a.Lp; t += kThreads) {
       const uint32_t k = t < a.cache ? keys[t] : ~fkey(s_out[t]);
-      const uint32_t hi = pass == 0 ? 0u : (k >> (shift + 8));
-      if (hi == hi_want) atomicAdd(&hist[(k >> shift) & 255], 1);
+      if (key_hi(k, shift + width) == want)
+        atomicAdd(&hist[wave * 256 + ((k >> shift) & (nb - 1))], 1);
     }
     __syncthreads();
-    if (tid == 0) {
-      int cum = 0;
-      const int rank = cut_rank;
-      for (int dg = 0; dg < 256; ++dg) {
-        const int c = hist[dg];
-        if (cum + c > rank) {
-          cut_key |= (uint32_t)dg << shift;
-          cut_rank = rank - cum;
-          cut_eq = c;
-          break;
-        }
-        cum += c;
+    if (tid < nb) {
+      int sum = 0;
+      for (int w = 0; w < kWaves; ++w) sum += hist[w * 256 + tid];
+      hist[tid] = sum;
+    }
+    __syncthreads();
+    if (wave == 0) {
+      int d, before, cnt;
+      wave_find_bin(hist, nb, crank, &d, &before, &cnt);
+      if (lane == 0) {
+        cut_key = ck | ((uint32_t)d << shift);
+        cut_rank = crank - before;
+        cut_eq = cnt;
       }
     }
     __syncthreads();
+    ck = cut_key;
+    crank = cut_rank;
+    ceq = cut_eq;
+    done += width;
   }
+  (void)ceq;
 
-  // ---- 3. ordered flag + compaction
-  const uint32_t ck = cut_key;
-  const int crank = cut_rank;
-  const bool ties = cut_eq > 1;
-  int32_t* out = a.idx + (size_t)layer * a.B;
-  int carry = 0, carry_eq = 0;
-  for (int base = 0; base < a.Lp; base += kThreads) {
-    const int t = base + tid;
+  // ---- 3. ordered compaction: each wave owns a contiguous token segment.
+  // Selected: key < ck, or key == ck among the first crank+1 such tokens.
+  const int seg = ((a.Lp + kWaves * 64 - 1) / (kWaves * 64)) * 64;
+  const int t0 = wave * seg, t1 = min(t0 + seg, a.Lp);
+  const uint64_t below = lane == 0 ? 0ull : (~0ull >> (64 - lane));
+  int n_strict = 0, n_eq = 0;
+  for (int base = t0; base < t1; base += 64) {
+    const int t = base + lane;
     uint32_t k = 0xFFFFFFFFu;
-    if (t < a.Lp) k = t < a.cache ? keys[t] : ~fkey(s_out[t]);
-    bool sel = (t < a.Lp) && (k < ck);
-    if (ties) {
-      const bool eq = (t < a.Lp) && (k == ck);
-      int tot;
-      const int pos = block_excl_count(eq, sh_cnt, &tot) + carry_eq;
-      carry_eq += tot;
-      sel = sel || (eq && pos <= crank);
-    } else {
-      sel = sel || ((t < a.Lp) && (k == ck));
-    }
-    int tot;
-    const int pos = block_excl_count(sel, sh_cnt, &tot) + carry;
-    carry += tot;
+    if (t < t1) k = t < a.cache ? keys[t] : ~fkey(s_out[t]);
+    n_strict += __popcll(__ballot(t < t1 && k < ck));
+    n_eq += __popcll(__ballot(t < t1 && k == ck));
+  }
+  if (lane == 0) { wsel[wave] = n_strict; weq[wave] = n_eq; }
+  __syncthreads();
+  int off = 0, eq_off = 0;
+  for (int w = 0; w < wave; ++w) {
+    off += wsel[w] + max(0, min(crank + 1 - eq_off, weq[w]));
+    eq_off += weq[w];
+  }
+  int32_t* out = a.idx + (size_t)layer * a.B;
+  for (int base = t0; base < t1; base += 64) {
+    const int t = base + lane;
+    uint32_t k = 0xFFFFFFFFu;
+    if (t < t1) k = t < a.cache ? keys[t] : ~fkey(s_out[t]);
+    const bool strict = t < t1 && k < ck;
+    const bool eq = t < t1 && k == ck;
+    const uint64_t meq = __ballot(eq);
+    const int eqpos = eq_off + __popcll(meq & below);
+    const bool sel = strict || (eq && eqpos <= crank);
+    const uint64_t msel = __ballot(sel);
+    const int pos = off + __popcll(msel & below);
     if (sel && pos < a.B) out[pos] = t;
+    off += __popcll(msel);
+    eq_off += __popcll(meq);
   }
 }
 
@@ -170,8 +219,13 @@ int launch_select(const Geometry& g, const starkv_params& p, const float* sbar,
     a.sframe[i] = spans[i].frame;
   }
   const size_t lds = (size_t)a.cache * sizeof(uint32_t);
-  hipFuncSetAttribute(reinterpret_cast<const void*>(&select_kernel),
-                      hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+  static bool configured = false;   // one-time, idempotent
+  if (!configured) {
+    hipFuncSetAttribute(reinterpret_cast<const void*>(&select_kernel),
+                        hipFuncAttributeMaxDynamicSharedMemorySize,
+                        (int)(kLdsKeys * sizeof(uint32_t)));
+    configured = true;
+  }
   select_kernel<<<g.n_layers, kThreads, lds, st>>>(a);
   return (int)hipGetLastError();
 }

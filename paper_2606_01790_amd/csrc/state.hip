@@ -9,10 +9,13 @@
 //
 // Equal-frequency binning ranks the visual tokens of a group by (value,
 // token index).  The bin edges are the K-1 order statistics at ranks
-// ceil(b N / K), found by an MSB-first radix select over order-preserving
-// 32-bit keys (8-bit digits, histograms in LDS).  A token's bin is the number
-// of edges at or below it.  Equal keys at an edge are split by token index
-// with an ordered block scan, so ties resolve exactly as the ranking defines.
+// ceil(b N / K), found together by one MSB-first radix select over
+// order-preserving 32-bit keys: the bits every key shares are skipped, the
+// first digit is 12 bits wide (one LDS histogram, block-wide scan), later
+// digits are 8 bits with one histogram per distinct edge prefix and one
+// wave scanning per edge.  A token's bin is the number of edges at or below
+// it; equal keys at an edge are split by token index with an ordered block
+// scan, so ties resolve exactly as the ranking defines.
 #include "device_common.h"
 #include "internal.h"
 
@@ -41,6 +44,11 @@ struct StatsArgs {
 };
 
 constexpr int kThreads = 1024;
+constexpr int kWaves = kThreads / 64;
+constexpr int kBatch = 8;                 // loads in flight per thread
+constexpr int kHistInts = 16384;          // 64 KiB: digit or joint histograms
+constexpr int kKeyCache = 20 * 1024;      // visual keys kept in LDS
+constexpr size_t kStatsLds = (size_t)kHistInts * 4 + (size_t)kKeyCache * 4;
 
 // visual index v (spans in token order) -> token, row, column, span
 __device__ inline void visual_token(const SpanSet& sp, int v, int* t, int* r, int* c, int* s) {
@@ -57,33 +65,58 @@ __device__ inline void visual_token(const SpanSet& sp, int v, int* t, int* r, in
 }
 
 __global__ __launch_bounds__(kThreads) void stats_kernel(StatsArgs a) {
-  __shared__ int hist[64 * 256];          // radix histograms, then joint counts
+  extern __shared__ __align__(16) unsigned char smem[];
+  int* hist = reinterpret_cast<int*>(smem);
+  uint32_t* kc = reinterpret_cast<uint32_t*>(smem + (size_t)kHistInts * 4);
   __shared__ uint32_t t_key[64];          // edge key of target b
-  __shared__ int t_rank[64];              // rank among equal keys
-  __shared__ int t_eq[64];                // elements with that key
+  __shared__ int t_rank[64];              // rank among keys sharing the prefix
+  __shared__ int t_eq[64];                // keys equal to the edge key
   __shared__ int t_u[64];                 // histogram slot of the target
+  __shared__ uint32_t n_key[64];          // first-digit results
+  __shared__ int n_rank[64], n_eq[64];
   __shared__ uint32_t u_hi[64];
   __shared__ int n_u;
   __shared__ int nb_s[64];
   __shared__ int nc_s[256];
-  __shared__ int sh_cnt[kThreads / 64];
+  __shared__ int sh_cnt[kWaves];
   __shared__ int carry_s[64];
-  __shared__ double red[kThreads / 64];
+  __shared__ uint32_t red_lo[kWaves], red_hi[kWaves];
+  __shared__ double red[kWaves];
 
   const int layer = blockIdx.y, g = blockIdx.x;
-  const int tid = threadIdx.x;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   float* scal = a.scal + (size_t)layer * a.sc;
 
   if (g == a.G) {   // ------------------------------------ entropy block
     const float* sb = a.sbar + (size_t)layer * a.Lp;
     double z = 0.0;
-    for (int t = tid; t < a.Lp; t += kThreads) z += (double)sb[t];
+    for (int t0 = tid; t0 < a.Lp; t0 += kBatch * kThreads) {
+      float v[kBatch];
+#pragma unroll
+      for (int u = 0; u < kBatch; ++u) {   // kBatch loads in flight
+        const int t = t0 + u * kThreads;
+        v[u] = t < a.Lp ? sb[t] : 0.f;
+      }
+#pragma unroll
+      for (int u = 0; u < kBatch; ++u) z += (double)v[u];
+    }
     z = block_sum_d(z, red);
     const double denom = z + (double)a.eps;
     double e = 0.0;
-    for (int t = tid; t < a.Lp; t += kThreads) {
-      const double p = (double)sb[t] / denom;
-      e += p * log(p + (double)a.eps);
+    for (int t0 = tid; t0 < a.Lp; t0 += kBatch * kThreads) {
+      float v[kBatch];
+#pragma unroll
+      for (int u = 0; u < kBatch; ++u) {
+        const int t = t0 + u * kThreads;
+        v[u] = t < a.Lp ? sb[t] : -1.f;
+      }
+#pragma unroll
+      for (int u = 0; u < kBatch; ++u) {
+        if (v[u] >= 0.f) {
+          const double p = (double)v[u] / denom;
+          e += p * log(p + (double)a.eps);
+        }
+      }
     }
     e = block_sum_d(e, red);
     if (tid == 0) {
@@ -98,62 +131,136 @@ __global__ __launch_bounds__(kThreads) void stats_kernel(StatsArgs a) {
   const int N = a.sp.off[a.sp.n];
   const int K = a.nbins;
   const int M = a.grid;
+  const bool cached = N <= kKeyCache;
   double mi = 0.0;
 
   if (N > 0) {
+    // ---- visual keys (LDS when they fit), min and max
+    uint32_t lo = 0xFFFFFFFFu, hi = 0u;
+    for (int s = 0; s < a.sp.n; ++s) {
+      const int n_s = a.sp.rows[s] * a.sp.cols[s];
+      const float* src = Sg + a.sp.start[s];
+      uint32_t* dst = kc + a.sp.off[s];
+      for (int i0 = tid; i0 < n_s; i0 += kBatch * kThreads) {
+        float v[kBatch];
+#pragma unroll
+        for (int u = 0; u < kBatch; ++u) {   // kBatch loads in flight
+          const int i = i0 + u * kThreads;
+          v[u] = i < n_s ? src[i] : 0.f;
+        }
+#pragma unroll
+        for (int u = 0; u < kBatch; ++u) {
+          const int i = i0 + u * kThreads;
+          if (i < n_s) {
+            const uint32_t k = fkey(v[u]);
+            if (cached) dst[i] = k;
+            lo = min(lo, k);
+            hi = max(hi, k);
+          }
+        }
+      }
+    }
+    lo = wave_min_u32(lo);
+    hi = wave_max_u32(hi);
+    if (lane == 0) { red_lo[wave] = lo; red_hi[wave] = hi; }
     // ---- edges: ranks ceil(b N / K), b = 1..K-1, that exist (rank < N)
     int n_t = 0;
     for (int b = 1; b < K; ++b)
       if (((int64_t)b * N + K - 1) / K < N) n_t = b;
+    __syncthreads();
+    uint32_t kmin = 0xFFFFFFFFu, kmax = 0u;
+    for (int w = 0; w < kWaves; ++w) { kmin = min(kmin, red_lo[w]); kmax = max(kmax, red_hi[w]); }
+    const int common = (kmin == kmax) ? 32 : __clz(kmin ^ kmax);
+    const uint32_t cmask = common == 0 ? 0u : (common >= 32 ? 0xFFFFFFFFu : (0xFFFFFFFFu << (32 - common)));
     if (tid < n_t) {
-      t_key[tid] = 0u;
+      t_key[tid] = kmin & cmask;
       t_rank[tid] = (int)(((int64_t)(tid + 1) * N + K - 1) / K);
+      t_eq[tid] = N;
     }
     __syncthreads();
-    for (int pass = 0; pass < 4; ++pass) {
-      const int shift = 24 - 8 * pass;
+    // ---- multi-target radix select: a 12-bit first digit (one histogram,
+    // every target shares the common prefix), then 8-bit digits with one
+    // histogram per distinct prefix
+    bool first = true;
+    for (int done = common; done < 32;) {
+      const int width = min(first ? 12 : 8, 32 - done);
+      const int shift = 32 - done - width;
+      const int nb = 1 << width;
       if (tid == 0) {   // distinct fixed prefixes share one histogram
         int nu = 0;
         for (int b = 0; b < n_t; ++b) {
-          const uint32_t hi = pass == 0 ? 0u : (t_key[b] >> (shift + 8));
+          const uint32_t h = key_hi(t_key[b], shift + width);
           int u = 0;
-          while (u < nu && u_hi[u] != hi) ++u;
-          if (u == nu) u_hi[nu++] = hi;
+          while (u < nu && u_hi[u] != h) ++u;
+          if (u == nu) u_hi[nu++] = h;
           t_u[b] = u;
         }
         n_u = nu;
       }
       __syncthreads();
       const int nu = n_u;
-      for (int i = tid; i < nu * 256; i += kThreads) hist[i] = 0;
+      for (int i = tid; i < nu * nb; i += kThreads) hist[i] = 0;
       __syncthreads();
       for (int s = 0; s < a.sp.n; ++s) {
         const int n_s = a.sp.rows[s] * a.sp.cols[s];
         const float* src = Sg + a.sp.start[s];
+        const uint32_t* kcs = kc + a.sp.off[s];
         for (int i = tid; i < n_s; i += kThreads) {
-          const uint32_t key = fkey(src[i]);
-          const uint32_t hi = pass == 0 ? 0u : (key >> (shift + 8));
+          const uint32_t key = cached ? kcs[i] : fkey(src[i]);
+          const uint32_t h = key_hi(key, shift + width);
           int u = 0;
-          while (u < nu && u_hi[u] != hi) ++u;
-          if (u < nu) atomicAdd(&hist[u * 256 + ((key >> shift) & 255)], 1);
+          while (u < nu && u_hi[u] != h) ++u;
+          if (u < nu) atomicAdd(&hist[u * nb + ((key >> shift) & (nb - 1))], 1);
         }
       }
       __syncthreads();
-      if (tid < n_t) {
-        const int* h = hist + t_u[tid] * 256;
-        int cum = 0, rank = t_rank[tid];
-        for (int dg = 0; dg < 256; ++dg) {
-          const int c = h[dg];
-          if (cum + c > rank) {
-            t_key[tid] |= (uint32_t)dg << shift;
-            t_rank[tid] = rank - cum;
-            t_eq[tid] = c;
-            break;
+      if (first) {
+        // block-wide scan over the single histogram: thread owns 4 bins
+        int c[4], sum = 0;
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          c[j] = (4 * tid + j < nb) ? hist[4 * tid + j] : 0;
+          sum += c[j];
+        }
+        int tot;
+        const int exc = block_excl_scan(sum, sh_cnt, &tot);
+        // results go to separate arrays: every thread must read the old
+        // ranks before any is replaced
+        for (int b = 0; b < n_t; ++b) {
+          const int r = t_rank[b];
+          if (exc <= r && r < exc + sum) {
+            int run = exc;
+            for (int j = 0; j < 4; ++j) {
+              if (r < run + c[j]) {
+                n_key[b] = t_key[b] | ((uint32_t)(4 * tid + j) << shift);
+                n_rank[b] = r - run;
+                n_eq[b] = c[j];
+                break;
+              }
+              run += c[j];
+            }
           }
-          cum += c;
+        }
+        __syncthreads();
+        if (tid < n_t) {
+          t_key[tid] = n_key[tid];
+          t_rank[tid] = n_rank[tid];
+          t_eq[tid] = n_eq[tid];
+        }
+      } else {
+        for (int b = wave; b < n_t; b += kWaves) {
+          int d, before, cnt;
+          wave_find_bin(hist + t_u[b] * nb, nb, t_rank[b], &d, &before, &cnt);
+          if (lane == 0) {
+            t_key[b] |= (uint32_t)d << shift;
+            t_rank[b] -= before;
+            t_eq[b] = cnt;
+          }
         }
       }
       __syncthreads();
+      done += width;
+      first = false;
     }
 
     // ---- joint histogram of (bin, cell), visual tokens in index order
@@ -169,7 +276,7 @@ __global__ __launch_bounds__(kThreads) void stats_kernel(StatsArgs a) {
       uint32_t key = 0u;
       if (v < N) {
         visual_token(a.sp, v, &t, &r, &c, &s);
-        key = fkey(Sg[t]);
+        key = cached ? kc[v] : fkey(Sg[t]);
       }
       int bin = 0;
       if (!any_tie) {
@@ -233,10 +340,10 @@ __global__ __launch_bounds__(kThreads) void stats_kernel(StatsArgs a) {
   const float* scur = Sg + a.sp.start[a.cur];
   double dot = 0.0, ns = 0.0, nm = 0.0;
   for (int i = tid; i < nf; i += kThreads) {
-    const double s = scur[i];
+    const double sv = scur[i];
     const double mv = reset ? 0.0 : (double)m[i];
-    dot += s * mv;
-    ns += s * s;
+    dot += sv * mv;
+    ns += sv * sv;
     nm += mv * mv;
   }
   dot = block_sum_d(dot, red);
@@ -260,47 +367,53 @@ struct FinalArgs {
 };
 
 __global__ __launch_bounds__(64) void finalize_kernel(FinalArgs a) {
-  if (threadIdx.x != 0) return;
-  const int layer = blockIdx.x;
+  // one lane per group (G <= 64); wave reductions in a fixed order
+  const int layer = blockIdx.x, lane = threadIdx.x;
   float* scal = a.scal + (size_t)layer * a.sc;
   char* blk = a.state + (size_t)layer * a.state_stride;
   StateHeader* hdr = reinterpret_cast<StateHeader*>(blk);
   float* mibar = reinterpret_cast<float*>(blk + sizeof(StateHeader));
   const int G = a.G;
-  double lo = 0.0, hi = 0.0;
-  for (int g = 0; g < G; ++g) {
-    const double v = (double)a.rho_mi * (double)mibar[g] +
-                     (1.0 - (double)a.rho_mi) * (double)scal[STARKV_SCAL_MI(G) + g];
-    mibar[g] = (float)v;
-    scal[STARKV_SCAL_MIBAR(G) + g] = (float)v;
-    lo = g == 0 ? v : fmin(lo, v);
-    hi = g == 0 ? v : fmax(hi, v);
+  const bool on = lane < G;
+  const int n_prev = hdr->n;
+  const float h = scal[STARKV_SCAL_HHAT(G)];
+  double v = 0.0;
+  if (on) {
+    v = (double)a.rho_mi * (double)mibar[lane] +
+        (1.0 - (double)a.rho_mi) * (double)scal[STARKV_SCAL_MI(G) + lane];
+    v = (double)(float)v;                 // the state keeps float32
   }
-  double zmax = -1e300, zs = 0.0;
-  for (int g = 0; g < G; ++g) {
-    const double z = (((double)mibar[g] - lo) / (hi - lo + (double)a.eps)) / (double)a.tau;
-    zmax = fmax(zmax, z);
+  double lo = on ? v : 1e300, hi = on ? v : -1e300;
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) {
+    lo = fmin(lo, __shfl_xor(lo, o));
+    hi = fmax(hi, __shfl_xor(hi, o));
   }
-  for (int g = 0; g < G; ++g) {
-    const double z = (((double)mibar[g] - lo) / (hi - lo + (double)a.eps)) / (double)a.tau;
-    zs += exp(z - zmax);
+  const double z = on ? ((v - lo) / (hi - lo + (double)a.eps)) / (double)a.tau : -1e300;
+  double zmax = z;
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) zmax = fmax(zmax, __shfl_xor(zmax, o));
+  const double ez = on ? exp(z - zmax) : 0.0;
+  const double zs = wave_sum_d(ez);
+  if (on) {
+    mibar[lane] = (float)v;
+    scal[STARKV_SCAL_MIBAR(G) + lane] = (float)v;
+    scal[STARKV_SCAL_W(G) + lane] = (float)(ez / zs);
   }
-  for (int g = 0; g < G; ++g) {
-    const double z = (((double)mibar[g] - lo) / (hi - lo + (double)a.eps)) / (double)a.tau;
-    scal[STARKV_SCAL_W(G) + g] = (float)(exp(z - zmax) / zs);
+  if (lane == 0) {
+    const int n = n_prev + 1;
+    double lam = 0.0;
+    if (n > a.n_warmup) {
+      lam = a.n_ramp <= 0 ? (double)a.lam
+                          : (double)a.lam * fmin(1.0, (double)(n - a.n_warmup) / (double)a.n_ramp);
+    }
+    scal[STARKV_SCAL_LAMBDA(G)] = (float)lam;
+    scal[STARKV_SCAL_T(G)] =
+        (float)((double)a.t_min + ((double)a.t_max - (double)a.t_min) * (double)h);
+    scal[STARKV_SCAL_N(G)] = (float)n;
+    hdr->n = n;
+    if (a.nf >= 0) hdr->nf = a.nf;
   }
-  const int n = hdr->n + 1;
-  double lam = 0.0;
-  if (n > a.n_warmup) {
-    lam = a.n_ramp <= 0 ? (double)a.lam
-                        : (double)a.lam * fmin(1.0, (double)(n - a.n_warmup) / (double)a.n_ramp);
-  }
-  scal[STARKV_SCAL_LAMBDA(G)] = (float)lam;
-  const double h = scal[STARKV_SCAL_HHAT(G)];
-  scal[STARKV_SCAL_T(G)] = (float)((double)a.t_min + ((double)a.t_max - (double)a.t_min) * h);
-  scal[STARKV_SCAL_N(G)] = (float)n;
-  hdr->n = n;
-  if (a.nf >= 0) hdr->nf = a.nf;
 }
 
 __global__ __launch_bounds__(256) void state_init_kernel(char* state, size_t stride,
@@ -352,7 +465,13 @@ int launch_update_state(const Geometry& g, const starkv_params& p,
     a.sp.frame[i] = spans[i].frame;
     a.sp.off[i + 1] = a.sp.off[i] + spans[i].rows * spans[i].cols;
   }
-  stats_kernel<<<dim3(g.G + 1, g.n_layers), kThreads, 0, st>>>(a);
+  static bool configured = false;   // one-time, idempotent
+  if (!configured) {
+    hipFuncSetAttribute(reinterpret_cast<const void*>(&stats_kernel),
+                        hipFuncAttributeMaxDynamicSharedMemorySize, (int)kStatsLds);
+    configured = true;
+  }
+  stats_kernel<<<dim3(g.G + 1, g.n_layers), kThreads, kStatsLds, st>>>(a);
   FinalArgs f;
   f.scal = scalars;
   f.state = a.state;

@@ -26,6 +26,7 @@ starkv_status check_dims(const starkv_dims* dims, Geometry* g) {
   const int64_t R = W * (H / G);
   const int64_t Rpad = (R + 31) / 32 * 32;
   if (Rpad > 512 || Rpad * (d * esz + 16) > kMaxQBytes) return STARKV_E_SHAPE;
+  if (esz == 4 && Rpad > 128) return STARKV_E_SHAPE;   // float32: up to 4 row blocks
   if (g) {
     g->n_layers = (int)nl;
     g->H = (int)H;
@@ -119,7 +120,8 @@ WsLayout ws_layout(const Geometry& g) {
   WsLayout w;
   const size_t lg = (size_t)g.n_layers * g.G;
   w.part_off = 0;
-  w.sraw_off = up256(lg * max_chunks(g) * g.Rpad * 2 * sizeof(float));
+  w.cst_off = up256(lg * max_chunks(g) * g.Rpad * 2 * sizeof(float));
+  w.sraw_off = w.cst_off + up256(lg * g.Rpad * sizeof(float));
   w.total = w.sraw_off + up256(lg * g.Lp * sizeof(float));
   return w;
 }

@@ -74,8 +74,10 @@ def test_sizes():
     ws = sk.workspace_bytes(d)
     Lp = 13711 - 32
     chunks = (Lp + 255) // 256
-    part = (28 * 4 * chunks * 224 * 8 + 255) // 256 * 256
-    assert ws == part + (28 * 4 * Lp * 4 + 255) // 256 * 256
+    up = lambda x: (x + 255) // 256 * 256  # noqa: E731
+    part = up(28 * 4 * chunks * 224 * 8)    # per-chunk row statistics
+    cst = up(28 * 4 * 224 * 4)              # merged row statistics
+    assert ws == part + cst + up(28 * 4 * Lp * 4)
     assert sk.workspace_bytes(dims(G=3)) == 0          # H % G != 0
 
 
