@@ -32,8 +32,8 @@ class Params:
     open carry the reading noted beside them."""
 
     lam: float = 0.5          # target MI prior strength lambda
-    n_warmup: int = 5         # "5 online profiling steps"
-    n_ramp: int = 10          # "10-step ramp for lambda_eff"
+    n_warmup: int = 5         # online profiling steps before the prior acts
+    n_ramp: int = 10          # steps over which lambda_eff ramps up to lambda
     rho_mi: float = 0.9       # MI EMA decay rho
     tau: float = 1.0          # prior softmax temperature
     rho_t: float = 0.9        # stability EMA decay rho_t

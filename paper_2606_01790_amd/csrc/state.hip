@@ -48,26 +48,25 @@ constexpr int kWaves = kThreads / 64;
 constexpr int kBatch = 8;                 // loads in flight per thread
 constexpr int kHistInts = 16384;          // 64 KiB: digit or joint histograms
 constexpr int kKeyCache = 20 * 1024;      // visual keys kept in LDS
-constexpr size_t kStatsLds = (size_t)kHistInts * 4 + (size_t)kKeyCache * 4;
+constexpr int kCand = 2048;               // keys in the edges' first-digit buckets
+constexpr size_t kStatsLds =
+    (size_t)kHistInts * 4 + (size_t)kKeyCache * 4 + (size_t)kCand * 4;
 
-// visual index v (spans in token order) -> token, row, column, span
-__device__ inline void visual_token(const SpanSet& sp, int v, int* t, int* r, int* c, int* s) {
-  int lo = 0, hi = sp.n - 1;
-  while (lo < hi) {           // last span with off <= v
-    const int mid = (lo + hi + 1) >> 1;
-    if (sp.off[mid] <= v) lo = mid; else hi = mid - 1;
-  }
-  const int i = v - sp.off[lo];
-  *s = lo;
-  *r = i / sp.cols[lo];
-  *c = i % sp.cols[lo];
-  *t = sp.start[lo] + i;
+// floor(x * M / n) for 0 <= x < n, without an integer division: the float
+// estimate is within one of the quotient (x * M < 2^31, M <= 16).
+__device__ inline int scaled_index(int x, int M, int n, float m_over_n) {
+  int q = (int)((float)x * m_over_n);
+  const int xm = x * M;
+  if (q * n > xm) --q;
+  else if ((q + 1) * n <= xm) ++q;
+  return q;
 }
 
 __global__ __launch_bounds__(kThreads) void stats_kernel(StatsArgs a) {
   extern __shared__ __align__(16) unsigned char smem[];
   int* hist = reinterpret_cast<int*>(smem);
   uint32_t* kc = reinterpret_cast<uint32_t*>(smem + (size_t)kHistInts * 4);
+  uint32_t* cand = kc + kKeyCache;
   __shared__ uint32_t t_key[64];          // edge key of target b
   __shared__ int t_rank[64];              // rank among keys sharing the prefix
   __shared__ int t_eq[64];                // keys equal to the edge key
@@ -75,7 +74,8 @@ __global__ __launch_bounds__(kThreads) void stats_kernel(StatsArgs a) {
   __shared__ uint32_t n_key[64];          // first-digit results
   __shared__ int n_rank[64], n_eq[64];
   __shared__ uint32_t u_hi[64];
-  __shared__ int n_u;
+  __shared__ int n_u, n_cand, cand_total;
+  __shared__ uint32_t bucket_bits[128];   // first-digit buckets holding an edge
   __shared__ int nb_s[64];
   __shared__ int nc_s[256];
   __shared__ int sh_cnt[kWaves];
@@ -180,37 +180,46 @@ __global__ __launch_bounds__(kThreads) void stats_kernel(StatsArgs a) {
     __syncthreads();
     // ---- multi-target radix select: a 12-bit first digit (one histogram,
     // every target shares the common prefix), then 8-bit digits with one
-    // histogram per distinct prefix
-    bool first = true;
+    // histogram per distinct prefix.  After the first digit the keys in the
+    // edges' buckets are compacted into LDS when they fit, and the later
+    // digits scan only those.
+    bool first = true, compact = false;
+    int n_c = 0;
     for (int done = common; done < 32;) {
       const int width = min(first ? 12 : 8, 32 - done);
       const int shift = 32 - done - width;
       const int nb = 1 << width;
-      if (tid == 0) {   // distinct fixed prefixes share one histogram
-        int nu = 0;
-        for (int b = 0; b < n_t; ++b) {
-          const uint32_t h = key_hi(t_key[b], shift + width);
-          int u = 0;
-          while (u < nu && u_hi[u] != h) ++u;
-          if (u == nu) u_hi[nu++] = h;
-          t_u[b] = u;
-        }
-        n_u = nu;
+      if (wave == 0) {
+        // targets ascend, so equal prefixes are adjacent: slot ids are a scan
+        // of "prefix differs from the previous target's"
+        const bool on = lane < n_t;
+        const uint32_t h = on ? key_hi(t_key[lane], shift + width) : 0u;
+        const uint32_t hp = (uint32_t)__shfl_up((int)h, 1);
+        const bool fresh = on && (lane == 0 || hp != h);
+        const int inc = wave_incl_scan(fresh ? 1 : 0);
+        if (on) t_u[lane] = inc - 1;
+        if (fresh) u_hi[inc - 1] = h;
+        if (lane == 63) n_u = inc;
       }
       __syncthreads();
       const int nu = n_u;
       for (int i = tid; i < nu * nb; i += kThreads) hist[i] = 0;
       __syncthreads();
-      for (int s = 0; s < a.sp.n; ++s) {
-        const int n_s = a.sp.rows[s] * a.sp.cols[s];
-        const float* src = Sg + a.sp.start[s];
-        const uint32_t* kcs = kc + a.sp.off[s];
-        for (int i = tid; i < n_s; i += kThreads) {
-          const uint32_t key = cached ? kcs[i] : fkey(src[i]);
-          const uint32_t h = key_hi(key, shift + width);
-          int u = 0;
-          while (u < nu && u_hi[u] != h) ++u;
-          if (u < nu) atomicAdd(&hist[u * nb + ((key >> shift) & (nb - 1))], 1);
+      auto count = [&](uint32_t key) {
+        const uint32_t h = key_hi(key, shift + width);
+        int u = 0;
+        while (u < nu && u_hi[u] != h) ++u;
+        if (u < nu) atomicAdd(&hist[u * nb + ((key >> shift) & (nb - 1))], 1);
+      };
+      if (compact) {
+        for (int i = tid; i < n_c; i += kThreads) count(cand[i]);
+      } else if (cached) {
+        for (int i = tid; i < N; i += kThreads) count(kc[i]);
+      } else {
+        for (int s = 0; s < a.sp.n; ++s) {
+          const int n_s = a.sp.rows[s] * a.sp.cols[s];
+          const float* src = Sg + a.sp.start[s];
+          for (int i = tid; i < n_s; i += kThreads) count(fkey(src[i]));
         }
       }
       __syncthreads();
@@ -241,11 +250,56 @@ __global__ __launch_bounds__(kThreads) void stats_kernel(StatsArgs a) {
             }
           }
         }
+        if (tid < 128) bucket_bits[tid] = 0u;
         __syncthreads();
         if (tid < n_t) {
           t_key[tid] = n_key[tid];
           t_rank[tid] = n_rank[tid];
           t_eq[tid] = n_eq[tid];
+          const uint32_t dg = (n_key[tid] >> shift) & (uint32_t)(nb - 1);
+          atomicOr(&bucket_bits[dg >> 5], 1u << (dg & 31));
+        }
+        if (wave == 0) {   // keys in the edges' buckets (distinct buckets once)
+          const bool on = lane < n_t;
+          const uint32_t dg = on ? ((n_key[lane] >> shift) & (uint32_t)(nb - 1)) : 0u;
+          const uint32_t dp = (uint32_t)__shfl_up((int)dg, 1);
+          const bool fresh = on && (lane == 0 || dp != dg);
+          int v = fresh ? n_eq[lane] : 0;
+#pragma unroll
+          for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o);
+          if (lane == 0) { cand_total = v; n_cand = 0; }
+        }
+        __syncthreads();
+        if (done + width < 32 && cand_total <= kCand) {
+          // compact them (order is irrelevant for counting)
+          auto keep = [&](uint32_t key, bool valid) {
+            const uint32_t dg = (key >> shift) & (uint32_t)(nb - 1);
+            const bool m = valid && ((bucket_bits[dg >> 5] >> (dg & 31)) & 1u);
+            const uint64_t bal = __ballot(m);
+            int base = 0;
+            if (lane == 0 && bal) base = atomicAdd(&n_cand, __popcll(bal));
+            base = __shfl(base, 0);
+            const uint64_t below = lane == 0 ? 0ull : (~0ull >> (64 - lane));
+            if (m) cand[base + __popcll(bal & below)] = key;
+          };
+          if (cached) {
+            for (int i0 = 0; i0 < N; i0 += kThreads) {
+              const int i = i0 + tid;
+              keep(i < N ? kc[i] : 0u, i < N);
+            }
+          } else {
+            for (int s = 0; s < a.sp.n; ++s) {
+              const int n_s = a.sp.rows[s] * a.sp.cols[s];
+              const float* src = Sg + a.sp.start[s];
+              for (int i0 = 0; i0 < n_s; i0 += kThreads) {
+                const int i = i0 + tid;
+                keep(i < n_s ? fkey(src[i]) : 0u, i < n_s);
+              }
+            }
+          }
+          __syncthreads();
+          compact = true;
+          n_c = n_cand;
         }
       } else {
         for (int b = wave; b < n_t; b += kWaves) {
@@ -263,43 +317,61 @@ __global__ __launch_bounds__(kThreads) void stats_kernel(StatsArgs a) {
       first = false;
     }
 
-    // ---- joint histogram of (bin, cell), visual tokens in index order
+    // ---- joint histogram of (bin, cell), spans in order, row-major inside
+    // a span (the visual-token order the ranking's tie rule refers to)
     const int ncell = M * M;
     for (int i = tid; i < K * ncell; i += kThreads) hist[i] = 0;
     bool any_tie = false;
     for (int b = 0; b < n_t; ++b) any_tie |= (t_eq[b] > 1);
     if (tid < 64) carry_s[tid] = 0;
+    uint32_t tk[8];
+#pragma unroll
+    for (int j = 0; j < 8; ++j) tk[j] = j < n_t ? t_key[j] : 0u;
     __syncthreads();
-    for (int base = 0; base < N; base += kThreads) {
-      const int v = base + tid;
-      int t = 0, r = 0, c = 0, s = 0;
-      uint32_t key = 0u;
-      if (v < N) {
-        visual_token(a.sp, v, &t, &r, &c, &s);
-        key = cached ? kc[v] : fkey(Sg[t]);
-      }
-      int bin = 0;
-      if (!any_tie) {
-        for (int b = 0; b < n_t; ++b) bin += (key >= t_key[b]);
-      } else {
-        for (int b = 0; b < n_t; ++b) {
-          if (t_eq[b] > 1) {   // uniform branch: ordered split of equal keys
-            const bool eq = (v < N) && (key == t_key[b]);
-            const int c0 = carry_s[b];
-            int tot;
-            const int pos = block_excl_count(eq, sh_cnt, &tot) + c0;
-            bin += (key > t_key[b]) || (eq && pos >= t_rank[b]);
-            __syncthreads();
-            if (tid == 0) carry_s[b] = c0 + tot;
-            __syncthreads();
+    for (int s = 0; s < a.sp.n; ++s) {
+      const int rows = a.sp.rows[s], cols = a.sp.cols[s];
+      const int n_s = rows * cols;
+      const uint32_t* kcs = kc + a.sp.off[s];
+      const float* src = Sg + a.sp.start[s];
+      const float fr = (float)M / (float)rows, fc = (float)M / (float)cols;
+      // (row, col) of token i0 + tid, advanced by kThreads per iteration
+      int r = tid / cols, c = tid - (tid / cols) * cols;
+      const int dq = kThreads / cols, dr = kThreads - dq * cols;
+      for (int i0 = 0; i0 < n_s; i0 += kThreads) {
+        const int i = i0 + tid;
+        const bool valid = i < n_s;
+        const uint32_t key = valid ? (cached ? kcs[i] : fkey(src[i])) : 0u;
+        int bin = 0;
+        if (!any_tie) {
+          if (n_t <= 8) {
+#pragma unroll
+            for (int j = 0; j < 8; ++j) bin += (j < n_t) & (key >= tk[j]);
           } else {
-            bin += (key >= t_key[b]);
+            for (int b = 0; b < n_t; ++b) bin += (key >= t_key[b]);
+          }
+        } else {
+          for (int b = 0; b < n_t; ++b) {
+            if (t_eq[b] > 1) {   // uniform branch: ordered split of equal keys
+              const bool eq = valid && (key == t_key[b]);
+              const int c0 = carry_s[b];
+              int tot;
+              const int pos = block_excl_count(eq, sh_cnt, &tot) + c0;
+              bin += (key > t_key[b]) || (eq && pos >= t_rank[b]);
+              __syncthreads();
+              if (tid == 0) carry_s[b] = c0 + tot;
+              __syncthreads();
+            } else {
+              bin += (key >= t_key[b]);
+            }
           }
         }
-      }
-      if (v < N) {
-        const int cell = (r * M / a.sp.rows[s]) * M + (c * M / a.sp.cols[s]);
-        atomicAdd(&hist[bin * ncell + cell], 1);
+        if (valid) {
+          const int cell = scaled_index(r, M, rows, fr) * M + scaled_index(c, M, cols, fc);
+          atomicAdd(&hist[bin * ncell + cell], 1);
+        }
+        c += dr;
+        r += dq;
+        if (c >= cols) { c -= cols; ++r; }
       }
     }
     __syncthreads();

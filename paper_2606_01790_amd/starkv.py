@@ -176,6 +176,15 @@ def _esz(dims):
     return 4 if dims.dtype == F32 else 2
 
 
+def _need_cache(t, dims, lay, what):
+    """The strided cache view must lie inside the tensor's storage."""
+    if t is None:
+        return
+    last = ((dims.n_layers - 1) * lay.layer_stride + (dims.G - 1) * lay.group_stride
+            + (dims.L - 1) * lay.token_stride + dims.d)
+    _need(t, last * _esz(dims), what)
+
+
 # ------------------------------------------------------------------ entry points
 
 def state_init(dims: Dims, state, frame_cap: int, stream=None):
@@ -188,6 +197,7 @@ def score(dims: Dims, params: Params, q, k, k_layout: KVLayout, S, sbar, gstar,
           ws, stream=None):
     nl, Lp = dims.n_layers, dims.Lp
     _need(q, nl * dims.H * dims.W * dims.d * _esz(dims), "q")
+    _need_cache(k, dims, k_layout, "k")
     _need(S, nl * dims.G * Lp * 4, "S")
     _need(sbar, nl * Lp * 4, "sbar")
     _need(gstar, nl * Lp, "gstar")
@@ -201,6 +211,8 @@ def score(dims: Dims, params: Params, q, k, k_layout: KVLayout, S, sbar, gstar,
 def update_state(dims: Dims, params: Params, S, sbar, spans, frame: int, state,
                  frame_cap: int, scalars, ws=None, stream=None):
     arr, n = spans_array(spans)
+    _need(S, dims.n_layers * dims.G * dims.Lp * 4, "S")
+    _need(sbar, dims.n_layers * dims.Lp * 4, "sbar")
     _need(scalars, dims.n_layers * scalars_count(dims) * 4, "scalars")
     _need(state, state_bytes(dims, frame_cap), "state")
     _check("starkv_update_state", lib().starkv_update_state(
@@ -212,6 +224,9 @@ def update_state(dims: Dims, params: Params, S, sbar, spans, frame: int, state,
 def select(dims: Dims, params: Params, sbar, gstar, scalars, spans, frame: int,
            B: int, s, idx, ws=None, stream=None):
     arr, n = spans_array(spans)
+    _need(sbar, dims.n_layers * dims.Lp * 4, "sbar")
+    _need(gstar, dims.n_layers * dims.Lp, "gstar")
+    _need(scalars, dims.n_layers * scalars_count(dims) * 4, "scalars")
     _need(s, dims.n_layers * dims.Lp * 4, "s")
     if B > 0:
         _need(idx, dims.n_layers * B * 4, "idx")
@@ -224,6 +239,10 @@ def select(dims: Dims, params: Params, sbar, gstar, scalars, spans, frame: int,
 def compact(dims: Dims, k, v, kv_layout: KVLayout, idx, B: int, k_out, v_out,
             stream=None):
     nbytes = dims.n_layers * dims.G * (B + dims.W) * dims.d * _esz(dims)
+    _need_cache(k, dims, kv_layout, "k")
+    _need_cache(v, dims, kv_layout, "v")
+    if B > 0:
+        _need(idx, dims.n_layers * B * 4, "idx")
     _need(k_out, nbytes, "k_out")
     _need(v_out, nbytes, "v_out")
     _check("starkv_compact", lib().starkv_compact(

@@ -1,0 +1,145 @@
+"""GPU parity of the online statistics (sec. 3.4-3.6) on synthetic score rows.
+
+starkv_update_state is fed score rows S built on the host, bypassing the
+scoring stage, so that the equal-frequency bin edges land where the
+selection has its harder paths: many distinct-but-close keys around an edge
+(more than the kernel compacts into LDS), runs of exactly equal keys that
+span frames (the tie rule orders them by token index), and more visual
+tokens than the kernel caches in LDS.  The oracle bins the same float32
+values, so both sides decide on identical numbers.
+"""
+
+import numpy as np
+import pytest
+
+torch = pytest.importorskip("torch")
+
+from oracle import starkv_oracle as O  # noqa: E402
+from paper_2606_01790_amd import starkv as sk  # noqa: E402
+
+pytestmark = pytest.mark.gpu
+
+
+def say(msg):
+    print(f"[stats] {msg}", flush=True)
+
+
+def layout(n_frames, rows, cols, gap=37, head=50, tail=100):
+    spans, t = [], head
+    for f in range(1, n_frames + 1):
+        spans.append((t, rows, cols, f))
+        t += rows * cols + gap
+    return spans, t - gap + tail
+
+
+def cluster_row(rng, Lp, vis, n_below, n_cluster, base=1e-4):
+    """Scores of one group: n_below visual tokens under `base`, n_cluster
+    tokens whose float32 keys sit within 8 ulps of `base` (so they share
+    every leading key bit but the last three, and repeat exactly), the rest
+    above it; text tokens random."""
+    row = rng.uniform(1e-3, 1e-2, Lp).astype(np.float32)
+    perm = rng.permutation(vis)
+    lo = perm[:n_below]
+    cl = perm[n_below:n_below + n_cluster]
+    hi = perm[n_below + n_cluster:]
+    row[lo] = rng.uniform(1e-5, 5e-5, lo.size).astype(np.float32)
+    bits = np.full(cl.size, np.float32(base).view(np.uint32), np.uint32)
+    bits += rng.integers(0, 8, cl.size).astype(np.uint32)
+    row[cl] = bits.view(np.float32)
+    row[hi] = rng.uniform(2e-4, 1e-2, hi.size).astype(np.float32)
+    return row
+
+
+def run_stats(tag, S_steps, sbar, spans, frame, p):
+    """S_steps: list of [n_layers, G, Lp] float32 score tensors, one per call
+    with the same spans; checks MI, phi and H^ of every call."""
+    n_layers, G, Lp = S_steps[0].shape
+    W = 8
+    dims = sk.make_dims(n_layers, 2 * G, G, 64, Lp + W, W, sk.BF16)
+    op = O.Params(n_bins=int(p.n_bins), grid=int(p.grid), rho_t=float(p.rho_t),
+                  eps=float(p.eps))
+    is_vis, fr, r, c, rows, cols = O.visual_metadata(spans, Lp)
+    vis = np.nonzero(is_vis)[0]
+    cells = O.spatial_cells(r[vis], c[vis], rows[vis], cols[vis], op.grid)
+    cur = [s for s in spans if s[3] == frame][0]
+    cur_tok = np.arange(cur[0], cur[0] + cur[1] * cur[2])
+    frame_cap = cur[1] * cur[2]
+    dev = torch.device("cuda:0")
+    state = torch.empty(sk.state_bytes(dims, frame_cap), dtype=torch.uint8, device=dev)
+    scal = torch.empty(n_layers * sk.scalars_count(dims), dtype=torch.float32, device=dev)
+    sbar_d = torch.from_numpy(np.ascontiguousarray(np.broadcast_to(sbar, (n_layers, Lp)))).to(dev)
+    say(f"{tag}: N={vis.size} G={G} layers={n_layers} steps={len(S_steps)}")
+    sk.state_init(dims, state, frame_cap)
+    m = np.zeros((n_layers, G, frame_cap))
+    h_or, _ = O.entropy_temperature(sbar.astype(np.float64), 0.75, 1.25, op.eps)
+    for step, S in enumerate(S_steps, 1):
+        S_d = torch.from_numpy(S).to(dev)
+        sk.update_state(dims, p, S_d, sbar_d, spans, frame, state, frame_cap, scal)
+        torch.cuda.synchronize()
+        sc = scal.cpu().numpy().reshape(n_layers, -1)
+        for layer in range(n_layers):
+            S64 = S[layer].astype(np.float64)
+            mi = np.array([O.plugin_mi(O.rank_bins(S64[g, vis], op.n_bins), cells,
+                                       op.n_bins, op.grid * op.grid) for g in range(G)])
+            phi, m[layer] = O.stability(S64[:, cur_tok], m[layer], op.rho_t, op.eps)
+            got_mi = sc[layer, 0:G]
+            got_phi = sc[layer, 3 * G:4 * G]
+            assert np.max(np.abs(got_mi - mi)) <= 1e-5, \
+                f"{tag} step{step} L{layer}: MI {got_mi} vs {mi}"
+            assert np.max(np.abs(got_phi - phi)) <= 1e-5, \
+                f"{tag} step{step} L{layer}: phi {got_phi} vs {phi}"
+            assert abs(sc[layer, 4 * G + 1] - h_or) <= 1e-5, f"{tag}: H^"
+    say(f"{tag}: ok")
+
+
+def test_edges_in_dense_key_clusters():
+    """Five 69x39 frames (N = 13455).  Group 0: 3000 near-equal keys at the
+    bottom hold the first edge (beyond the LDS candidate list); group 1: 1500
+    of them hold the second edge (within it); group 2: exact ties only,
+    every key one of two values; group 3: plain random scores."""
+    rng = np.random.default_rng(7)
+    spans, Lp = layout(5, 39, 69)
+    is_vis = O.visual_metadata(spans, Lp)[0]
+    vis = np.nonzero(is_vis)[0]
+    steps = []
+    for _ in range(2):
+        S = np.empty((2, 4, Lp), np.float32)
+        for layer in range(2):
+            S[layer, 0] = cluster_row(rng, Lp, vis, 0, 3000)
+            S[layer, 1] = cluster_row(rng, Lp, vis, 3000, 1500)
+            S[layer, 2] = np.where(rng.random(Lp) < 0.5, 1e-3, 2e-3).astype(np.float32)
+            S[layer, 3] = rng.lognormal(-7, 1.5, Lp).astype(np.float32)
+        steps.append(S)
+    sbar = rng.uniform(1e-4, 1e-2, Lp).astype(np.float32)
+    run_stats("clusters", steps, sbar, spans, 5, sk.params_default())
+
+
+def test_visual_tokens_beyond_lds_cache():
+    """Six 51x69 frames (N = 21114, more keys than the LDS cache): keys are
+    re-read from S for every pass, with and without compaction."""
+    rng = np.random.default_rng(8)
+    spans, Lp = layout(6, 51, 69)
+    is_vis = O.visual_metadata(spans, Lp)[0]
+    vis = np.nonzero(is_vis)[0]
+    S = np.empty((1, 3, Lp), np.float32)
+    S[0, 0] = cluster_row(rng, Lp, vis, 2000, 1000)
+    S[0, 1] = cluster_row(rng, Lp, vis, 0, 4000)
+    S[0, 2] = rng.lognormal(-7, 1.5, Lp).astype(np.float32)
+    sbar = rng.uniform(1e-4, 1e-2, Lp).astype(np.float32)
+    run_stats("uncached", [S, S * np.float32(1.5)], sbar, spans, 6, sk.params_default())
+
+
+def test_many_bins_fine_grid():
+    """K = 64 equal-frequency bins on a 16 x 16 grid (the largest joint
+    histogram) with a dense cluster across several edges."""
+    rng = np.random.default_rng(9)
+    spans, Lp = layout(3, 40, 70)
+    is_vis = O.visual_metadata(spans, Lp)[0]
+    vis = np.nonzero(is_vis)[0]
+    S = np.empty((1, 2, Lp), np.float32)
+    S[0, 0] = cluster_row(rng, Lp, vis, 500, 2500)
+    S[0, 1] = rng.lognormal(-7, 1.5, Lp).astype(np.float32)
+    p = sk.params_default()
+    p.n_bins, p.grid = 64, 16
+    sbar = rng.uniform(1e-4, 1e-2, Lp).astype(np.float32)
+    run_stats("K64 M16", [S], sbar, spans, 3, p)
