@@ -38,13 +38,17 @@ def parse():
     ap.add_argument("--steps", type=int, default=30)
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--config", type=int, default=3)
-    ap.add_argument("--cpu-layers", type=int, default=6,
-                    help="layers in the oracle's timed sample (all trajectory steps)")
+    ap.add_argument("--cpu-seconds", type=float, default=10.0,
+                    help="oracle time of the CPU sample: layers are added, each with its "
+                         "whole trajectory, until this much oracle time has run")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--eager", action="store_true",
                     help="launch every call from Python instead of replaying a HIP graph")
     ap.add_argument("--copy-calibration", action="store_true",
-                    help="also run one plain 1 GiB device copy (counter calibration)")
+                    help="also run one plain elementwise kernel that reads 1 GiB and "
+                         "writes 1 GiB (the calibration of the HBM byte counters)")
+    ap.add_argument("--no-per-call", action="store_true",
+                    help="skip the per-call timing (no roofline; for counter runs)")
     return ap.parse_args()
 
 
@@ -256,23 +260,26 @@ def main():
     ms_per_step = max(gpu_ms, wall * 1e3) / args.steps
     value = layer_tokens / (ms_per_step * 1e-3)
 
-    log("per-call timing: graphs of back-to-back launches of one call")
-    per = per_call_timing(wl, spec, sk, torch, reps=10)
-    dom = max(per, key=lambda n: per[n]["time"])
-    dd = per[dom]
-    avg_s = dd["time"] / dd["launches"]
-    avg_b = dd["bytes"] / dd["launches"]
-    achieved = avg_b / avg_s / 1e9
-    roofline = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS,
-                "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
-                "traffic": None, "kernel": f"starkv_{dom}",
-                "avg_launch_us": round(avg_s * 1e6, 2),
-                "alg_bytes_per_launch": int(avg_b)}
-    per_call_us = {n: round(per[n]["time"] / per[n]["launches"] * 1e6, 2) for n in per}
+    roofline, per_call_us = None, None
+    if not args.no_per_call:
+        log("per-call timing: graphs of back-to-back launches of one call")
+        per = per_call_timing(wl, spec, sk, torch, reps=10)
+        dom = max(per, key=lambda n: per[n]["time"])
+        dd = per[dom]
+        avg_s = dd["time"] / dd["launches"]
+        avg_b = dd["bytes"] / dd["launches"]
+        achieved = avg_b / avg_s / 1e9
+        roofline = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS,
+                    "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
+                    "traffic": measured_traffic(f"starkv_{dom}", spec.name),
+                    "kernel": f"starkv_{dom}",
+                    "avg_launch_us": round(avg_s * 1e6, 2),
+                    "alg_bytes_per_launch": int(avg_b)}
+        per_call_us = {n: round(per[n]["time"] / per[n]["launches"] * 1e6, 2) for n in per}
 
     cpu = None
     if not args.no_cpu_baseline:
-        cpu = cpu_baseline(spec, params, args.cpu_layers)
+        cpu = cpu_baseline(spec, params, args.cpu_seconds)
 
     line = {
         "metric": METRIC,
@@ -299,19 +306,57 @@ def main():
         "cpu_baseline": cpu,
     }
     if args.copy_calibration:
-        n = 1 << 30
-        a = torch.empty(n, dtype=torch.uint8, device="cuda")
+        n = 1 << 28                       # float32: 1 GiB read, 1 GiB written
+        a = torch.ones(n, dtype=torch.float32, device="cuda")
         b = torch.empty_like(a)
-        b.copy_(a)
+        torch.neg(a, out=b)
         torch.cuda.synchronize()
-        line["copy_calibration_bytes"] = n
+        line["copy_calibration_bytes"] = 4 * n
     print(json.dumps(line), flush=True)
 
 
-def cpu_baseline(spec, params, n_layers_sample):
-    """The fp64 oracle, untuned, on the host: every trajectory step of the
-    first `n_layers_sample` layers (a layer-tokens/s rate, like the metric)."""
-    import numpy as np
+# Sources whose kernels the committed traffic figure was measured on.
+TRAFFIC_SOURCES = {
+    "starkv_score": ["score_kernels.h", "score.hip", "score_bf16.hip", "device_common.h"],
+}
+
+
+def sources_sha1(call):
+    import hashlib
+    h = hashlib.sha1()
+    for f in TRAFFIC_SOURCES.get(call, []):
+        with open(os.path.join(ROOT, "paper_2606_01790_amd", "csrc", f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()
+
+
+def measured_traffic(call, workload):
+    """HBM bytes per launch of `call` from the committed rocprofv3 FETCH_SIZE
+    and WRITE_SIZE summary of this workload, or None when there is none or
+    the call's kernel sources changed since the counters were taken."""
+    path = os.path.join(ROOT, "profiles", f"{call}-{workload}.traffic.md")
+    if call not in TRAFFIC_SOURCES or not os.path.exists(path):
+        return None
+    vals = {}
+    with open(path) as fh:
+        for ln in fh:
+            if ln.startswith("- ") and ":" in ln:
+                k, v = ln[2:].split(":", 1)
+                vals[k.strip()] = v.strip().strip("`")
+    if vals.get("sources_sha1") != sources_sha1(call):
+        return None
+    try:
+        return int(vals["traffic_bytes_per_launch"])
+    except (KeyError, ValueError):
+        return None
+
+
+def cpu_baseline(spec, params, seconds):
+    """The fp64 oracle, untuned, on the host cores: whole trajectories (every
+    step, fresh state) of layers 0, 1, 2, ... of the same workload, cycling
+    through the layers again if needed, until `seconds` of oracle time have
+    run.  Input generation is outside the timed part.  Reported as
+    layer-tokens/s, like the metric."""
     from oracle import starkv_oracle as O
     from paper_2606_01790_amd import workload as WL
 
@@ -328,28 +373,28 @@ def cpu_baseline(spec, params, n_layers_sample):
                   t_max=params.t_max, n_bins=params.n_bins, grid=params.grid,
                   pool_kernel=params.pool_kernel, eps=params.eps)
     tr = WL.Trajectory(spec)
-    nl = min(n_layers_sample, spec.n_layers)
-    inputs = []
-    for layer in range(nl):
+    log(f"cpu baseline: oracle trajectories until {seconds:.0f} s of oracle time")
+    spent, tokens, runs, layer = 0.0, 0, 0, 0
+    while spent < seconds:
+        steps = []
         for s in range(1, spec.steps + 1):
             K, V = tr.layer_cache(layer, s)
-            inputs.append((layer, s, WL.to_float64(tr.window_q(layer, s), spec.dtype),
-                           WL.to_float64(K, spec.dtype), K, V))
-    states = {l: O.LayerState(spec.G) for l in range(nl)}
-    log(f"cpu baseline: oracle on {nl} layers x {spec.steps} steps")
-    t0 = time.perf_counter()
-    tokens = 0
-    for layer, s, Q, K64, K, V in inputs:
-        _, states[layer] = O.compress_layer(Q, K64, None, spec.L(s), spec.W, spec.spans(s),
-                                            s, spec.budgets(s)[0], op, states[layer],
-                                            copy_rows=(K, V))
-        tokens += spec.n_vis(s)
-    dt = time.perf_counter() - t0
-    return {"value": round(tokens / dt, 1), "unit": "layer-tokens/s", "cores": threads,
+            steps.append((s, WL.to_float64(tr.window_q(layer, s), spec.dtype),
+                          WL.to_float64(K, spec.dtype), K, V))
+        state = O.LayerState(spec.G)
+        t0 = time.perf_counter()
+        for s, Q, K64, K, V in steps:
+            _, state = O.compress_layer(Q, K64, None, spec.L(s), spec.W, spec.spans(s), s,
+                                        spec.budgets(s)[0], op, state, copy_rows=(K, V))
+            tokens += spec.n_vis(s)
+        spent += time.perf_counter() - t0
+        runs += 1
+        layer = (layer + 1) % spec.n_layers
+    return {"value": round(tokens / spent, 1), "unit": "layer-tokens/s", "cores": threads,
             "kind": "oracle",
-            "sample": f"layers 0-{nl - 1}, all {spec.steps} trajectory steps "
-                      f"({tokens} layer-tokens, {dt:.1f} s, numpy fp64, BLAS threads "
-                      f"{threads})"}
+            "sample": f"{runs} whole {spec.steps}-step layer trajectories of {spec.name} "
+                      f"(layers 0-{min(runs, spec.n_layers) - 1}; {tokens} layer-tokens, "
+                      f"{spent:.1f} s of oracle time; numpy fp64, BLAS threads {threads})"}
 
 
 if __name__ == "__main__":

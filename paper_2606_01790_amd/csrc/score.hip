@@ -1,21 +1,6 @@
-// Window attention scoring (sec. 3.3): launch sequence, pooling and group
-// aggregation.  The MFMA passes live in score_kernels.h.
-//
-// Window attention scoring (sec. 3.3): A_raw summed over the window rows and
-// the heads of each KV group, then AvgPool1D, group mean, sbar and g*.
-//
-// The window softmax of every query row needs that row's max and sum over
-// all L_p past keys before any key's normalised mass is known, so scoring
-// runs in two passes over K:
-//   pass 1  per (layer, group, token chunk): for each window row r, the
-//           chunk's max M_r and sum of 2^(y - M_r), y = q.k * log2(e)/sqrt(d);
-//   pass 2  merges the chunk statistics into c_r = M_r + log2(l_r) and sums
-//           2^(y_rt - c_r) over the group's rows for every token t.
-// Both passes run the Q_g x K^T contraction on 32x32 MFMA tiles: the R = W*H/G
-// window rows of group g sit in LDS, K rows stream straight from HBM into
-// MFMA fragments.  Pass 1 puts tokens on the MFMA M axis, so each lane owns one
-// query row and reduces over its tokens in registers.  Pass 2 puts query rows
-// on M, so each lane owns one token and reduces over its rows in registers.
+// Window attention scoring (sec. 3.3, Eqs. A_raw and base_score): launch
+// sequence, pooling and group aggregation.  The two MFMA passes and the
+// merge of their row statistics live in score_kernels.h.
 #include <algorithm>
 
 #include "score_kernels.h"
