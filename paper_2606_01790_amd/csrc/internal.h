@@ -53,7 +53,8 @@ struct StateHeader {
   int32_t frame_cap;
   int32_t n;          // compression calls so far in this trajectory
   int32_t nf;         // token count of the frame m_g was built from
-  int32_t pad[11];
+  int32_t arrive;     // blocks of the running update that have finished
+  int32_t pad[10];
 };
 constexpr int32_t kStateMagic = 0x53544B56;  // "STKV"
 size_t state_stride(int G, int frame_cap);

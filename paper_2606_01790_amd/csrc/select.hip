@@ -1,11 +1,14 @@
 // Final score and global top-B (Eq. final_score, sec. 3.2; sec. 3.5 discount;
 // sec. 3.7 selection).  One 1024-thread workgroup per layer:
 //   1. s_t = max(sbar_t * beta_t * D_t, 0)^(1/T) for every past token,
-//      written out and kept as a descending-order key in LDS;
+//      written out and kept as a descending-order key in LDS (the span of a
+//      token comes from an LDS copy of the span table, walked by a cursor
+//      since each thread's tokens ascend);
 //   2. MSB-first radix select of the B-th key in the order (s descending,
-//      token index ascending): the bits every key shares are skipped, then
-//      8-bit digits are counted in per-wave LDS histograms and the digit is
-//      found with a wave-wide prefix scan;
+//      token index ascending): the bits every key shares are skipped, the
+//      first digit is 12 bits wide (one histogram, block-wide scan); the keys
+//      in the cut's bucket are then compacted into LDS when they fit and the
+//      later 8-bit digits count only those;
 //   3. ordered compaction: each wave owns a contiguous token segment, counts
 //      its selected tokens (keys past the cut, plus the lowest-index ties at
 //      the cut) with ballots, and writes them at its segment's offset, so idx
@@ -20,6 +23,7 @@ constexpr int kThreads = 1024;
 constexpr int kWaves = kThreads / 64;
 constexpr int kBatch = 8;              // loads in flight per thread
 constexpr int kLdsKeys = 28 * 1024;   // keys cached in LDS (112 KiB)
+constexpr int kCand = 2048;           // keys of the cut's first-digit bucket
 
 struct SelArgs {
   const float* sbar;
@@ -35,20 +39,14 @@ struct SelArgs {
   int32_t sframe[STARKV_MAX_SPANS];
 };
 
-// Span holding token t, or -1 (spans sorted by start, disjoint).
-__device__ inline int find_span(const SelArgs& a, int t) {
-  if (a.n_spans == 0 || t < a.start[0]) return -1;
-  int lo = 0, hi = a.n_spans - 1;
-  while (lo < hi) {
-    const int mid = (lo + hi + 1) >> 1;
-    if (a.start[mid] <= t) lo = mid; else hi = mid - 1;
-  }
-  return t < a.end[lo] ? lo : -1;
-}
-
 __global__ __launch_bounds__(kThreads) void select_kernel(SelArgs a) {
   extern __shared__ __align__(16) uint32_t keys[];
-  __shared__ int hist[kWaves * 256];      // per-wave digit histograms
+  __shared__ int hist[4096];              // first digit; later per-wave digits
+  __shared__ uint32_t cand[kCand];
+  __shared__ int sp_start[STARKV_MAX_SPANS], sp_end[STARKV_MAX_SPANS];
+  __shared__ float sp_dist[STARKV_MAX_SPANS];
+  __shared__ int sh_cnt[kWaves];
+  __shared__ int n_cand;
   __shared__ float w_s[STARKV_MAX_GROUPS], phi_s[STARKV_MAX_GROUPS];
   __shared__ uint32_t red_lo[kWaves], red_hi[kWaves];
   __shared__ uint32_t cut_key;
@@ -65,6 +63,11 @@ __global__ __launch_bounds__(kThreads) void select_kernel(SelArgs a) {
     w_s[tid] = scal[STARKV_SCAL_W(a.G) + tid];
     phi_s[tid] = scal[STARKV_SCAL_PHI(a.G) + tid];
   }
+  if (tid < a.n_spans) {
+    sp_start[tid] = a.start[tid];
+    sp_end[tid] = a.end[tid];
+    sp_dist[tid] = (float)(a.frame - a.sframe[tid]);
+  }
   __syncthreads();
   const float lam = scal[STARKV_SCAL_LAMBDA(a.G)];
   const float T = scal[STARKV_SCAL_T(a.G)];
@@ -73,6 +76,7 @@ __global__ __launch_bounds__(kThreads) void select_kernel(SelArgs a) {
 
   // ---- 1. fused score; keys order tokens by descending s
   uint32_t lo = 0xFFFFFFFFu, hi = 0u;
+  int cur = 0;   // first span that does not end at or before this thread's token
   for (int t0 = tid; t0 < a.Lp; t0 += kBatch * kThreads) {
     float sbv[kBatch];
     int gv[kBatch];
@@ -89,11 +93,9 @@ __global__ __launch_bounds__(kThreads) void select_kernel(SelArgs a) {
         const int g = min(gv[u], a.G - 1);
         const float beta = (1.0f - lam) + gl * w_s[g];
         float D = 1.0f;
-        const int sp = find_span(a, t);
-        if (sp >= 0) {
-          const float dist = (float)(a.frame - a.sframe[sp]);
-          D = a.d_min + (1.0f - a.d_min) * __expf(-a.delta * dist * phi_s[g]);
-        }
+        while (cur < a.n_spans && sp_end[cur] <= t) ++cur;
+        if (cur < a.n_spans && sp_start[cur] <= t)
+          D = a.d_min + (1.0f - a.d_min) * __expf(-a.delta * sp_dist[cur] * phi_s[g]);
         const float sf = fmaxf(sbv[u] * beta * D, 0.0f);
         const float sv = (inv_t == 1.0f || sf == 0.0f) ? sf : exp2f(inv_t * __log2f(sf));
         s_out[t] = sv;
@@ -116,42 +118,104 @@ __global__ __launch_bounds__(kThreads) void select_kernel(SelArgs a) {
   const int common = (kmin == kmax) ? 32 : __clz(kmin ^ kmax);
   const uint32_t cmask = common == 0 ? 0u : (common >= 32 ? 0xFFFFFFFFu : (0xFFFFFFFFu << (32 - common)));
   uint32_t ck = kmin & cmask;
-  int crank = a.B - 1, ceq = a.Lp;
+  int crank = a.B - 1;
+  bool first = true, compact = false;
+  int n_c = 0;
   for (int done = common; done < 32;) {
-    const int width = min(8, 32 - done);
+    const int width = min(first ? 12 : 8, 32 - done);
     const int shift = 32 - done - width;
     const int nb = 1 << width;
-    for (int i = tid; i < kWaves * 256; i += kThreads) hist[i] = 0;
-    __syncthreads();
     const uint32_t want = key_hi(ck, shift + width);
-    for (int t = tid; t < a.Lp; t += kThreads) {
-      const uint32_t k = t < a.cache ? keys[t] : ~fkey(s_out[t]);
-      if (key_hi(k, shift + width) == want)
-        atomicAdd(&hist[wave * 256 + ((k >> shift) & (nb - 1))], 1);
-    }
-    __syncthreads();
-    if (tid < nb) {
-      int sum = 0;
-      for (int w = 0; w < kWaves; ++w) sum += hist[w * 256 + tid];
-      hist[tid] = sum;
-    }
-    __syncthreads();
-    if (wave == 0) {
-      int d, before, cnt;
-      wave_find_bin(hist, nb, crank, &d, &before, &cnt);
-      if (lane == 0) {
-        cut_key = ck | ((uint32_t)d << shift);
-        cut_rank = crank - before;
-        cut_eq = cnt;
+    if (first) {
+      for (int i = tid; i < nb; i += kThreads) hist[i] = 0;
+      __syncthreads();
+      // every key shares the prefix: one histogram of the first digit
+      for (int t = tid; t < a.Lp; t += kThreads) {
+        const uint32_t k = t < a.cache ? keys[t] : ~fkey(s_out[t]);
+        atomicAdd(&hist[(k >> shift) & (nb - 1)], 1);
       }
+      __syncthreads();
+      int c[4], sum = 0;
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        c[j] = (4 * tid + j < nb) ? hist[4 * tid + j] : 0;
+        sum += c[j];
+      }
+      int tot;
+      const int exc = block_excl_scan(sum, sh_cnt, &tot);
+      if (exc <= crank && crank < exc + sum) {
+        int run = exc;
+        for (int j = 0; j < 4; ++j) {
+          if (crank < run + c[j]) {
+            cut_key = ck | ((uint32_t)(4 * tid + j) << shift);
+            cut_rank = crank - run;
+            cut_eq = c[j];
+            break;
+          }
+          run += c[j];
+        }
+      }
+      if (tid == 0) n_cand = 0;
+      __syncthreads();
+      ck = cut_key;
+      crank = cut_rank;
+      if (done + width < 32 && cut_eq <= kCand) {
+        // the keys of the cut's bucket, in any order
+        const uint32_t pre = key_hi(ck, shift);
+        const uint64_t below = lane == 0 ? 0ull : (~0ull >> (64 - lane));
+        for (int t0 = 0; t0 < a.Lp; t0 += kThreads) {
+          const int t = t0 + tid;
+          const uint32_t k = t < a.Lp ? (t < a.cache ? keys[t] : ~fkey(s_out[t])) : 0u;
+          const bool m = t < a.Lp && key_hi(k, shift) == pre;
+          const uint64_t bal = __ballot(m);
+          int base = 0;
+          if (lane == 0 && bal) base = atomicAdd(&n_cand, __popcll(bal));
+          base = __shfl(base, 0);
+          if (m) cand[base + __popcll(bal & below)] = k;
+        }
+        __syncthreads();
+        compact = true;
+        n_c = n_cand;
+      }
+    } else {
+      for (int i = tid; i < kWaves * 256; i += kThreads) hist[i] = 0;
+      __syncthreads();
+      if (compact) {
+        for (int i = tid; i < n_c; i += kThreads) {
+          const uint32_t k = cand[i];
+          if (key_hi(k, shift + width) == want)
+            atomicAdd(&hist[wave * 256 + ((k >> shift) & (nb - 1))], 1);
+        }
+      } else {
+        for (int t = tid; t < a.Lp; t += kThreads) {
+          const uint32_t k = t < a.cache ? keys[t] : ~fkey(s_out[t]);
+          if (key_hi(k, shift + width) == want)
+            atomicAdd(&hist[wave * 256 + ((k >> shift) & (nb - 1))], 1);
+        }
+      }
+      __syncthreads();
+      if (tid < nb) {
+        int sum = 0;
+        for (int w = 0; w < kWaves; ++w) sum += hist[w * 256 + tid];
+        hist[tid] = sum;
+      }
+      __syncthreads();
+      if (wave == 0) {
+        int d, before, cnt;
+        wave_find_bin(hist, nb, crank, &d, &before, &cnt);
+        if (lane == 0) {
+          cut_key = ck | ((uint32_t)d << shift);
+          cut_rank = crank - before;
+          cut_eq = cnt;
+        }
+      }
+      __syncthreads();
+      ck = cut_key;
+      crank = cut_rank;
     }
-    __syncthreads();
-    ck = cut_key;
-    crank = cut_rank;
-    ceq = cut_eq;
     done += width;
+    first = false;
   }
-  (void)ceq;
 
   // ---- 3. ordered compaction: each wave owns a contiguous token segment.
   // Selected: key < ck, or key == ck among the first crank+1 such tokens.

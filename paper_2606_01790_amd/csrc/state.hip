@@ -1,11 +1,13 @@
 // Online statistics of one step (sec. 3.4-3.6).
 //
-// stats kernel, grid (G + 1, n_layers), 1024 threads:
-//   block g < G   spatial MI of group g (sec. 3.4, Eq. MI) and its stability
-//                 phi_g with the stability-mean update (sec. 3.5);
-//   block G       normalised entropy H^ of sbar (sec. 3.6).
-// finalize kernel, one wave per layer: MI EMA, min-max prior w, lambda
-// schedule, temperature T, state bookkeeping.
+// stats kernel, grid (G + 2, n_layers), 1024 threads:
+//   block g < G   spatial MI of group g (sec. 3.4, Eq. MI);
+//   block G       normalised entropy H^ of sbar (sec. 3.6);
+//   block G + 1   stability phi_g of every group with the stability-mean
+//                 update (sec. 3.5).
+// The last block of each layer to finish then runs the layer's finalize in
+// one wave: MI EMA, min-max prior w, lambda schedule, temperature T, state
+// bookkeeping.
 //
 // Equal-frequency binning ranks the visual tokens of a group by (value,
 // token index).  The bin edges are the K-1 order statistics at ranks
@@ -31,6 +33,15 @@ struct SpanSet {
   int32_t off[STARKV_MAX_SPANS + 1];   // visual tokens before span i
 };
 
+struct FinalArgs {
+  float* scal;
+  char* state;
+  size_t state_stride;
+  int G, sc, nf;      // nf = current frame tokens, or -1
+  float rho_mi, tau, eps, lam, t_min, t_max;
+  int n_warmup, n_ramp;
+};
+
 struct StatsArgs {
   const float* S;
   const float* sbar;
@@ -41,6 +52,7 @@ struct StatsArgs {
   int G, Lp, nbins, grid, cur, frame_cap, sc;
   float rho_t, eps;
   SpanSet sp;
+  FinalArgs fin;          // the layer's finalize, run by its last block
 };
 
 constexpr int kThreads = 1024;
@@ -62,7 +74,7 @@ __device__ inline int scaled_index(int x, int M, int n, float m_over_n) {
   return q;
 }
 
-__global__ __launch_bounds__(kThreads) void stats_kernel(StatsArgs a) {
+__device__ void stats_body(const StatsArgs& a) {
   extern __shared__ __align__(16) unsigned char smem[];
   int* hist = reinterpret_cast<int*>(smem);
   uint32_t* kc = reinterpret_cast<uint32_t*>(smem + (size_t)kHistInts * 4);
@@ -82,6 +94,7 @@ __global__ __launch_bounds__(kThreads) void stats_kernel(StatsArgs a) {
   __shared__ int carry_s[64];
   __shared__ uint32_t red_lo[kWaves], red_hi[kWaves];
   __shared__ double red[kWaves];
+  __shared__ double red12[kWaves][12];
 
   const int layer = blockIdx.y, g = blockIdx.x;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -123,6 +136,71 @@ __global__ __launch_bounds__(kThreads) void stats_kernel(StatsArgs a) {
       double h = 0.0;
       if (a.Lp > 1) h = fmin(1.0, fmax(0.0, -e / log((double)a.Lp)));
       scal[STARKV_SCAL_HHAT(a.G)] = (float)h;
+    }
+    return;
+  }
+
+  if (g == a.G + 1) {   // ---------------------------------- stability block
+    if (a.cur < 0) {
+      for (int j = tid; j < a.G; j += kThreads) scal[STARKV_SCAL_PHI(a.G) + j] = 0.f;
+      return;
+    }
+    char* blk = a.state + (size_t)layer * a.state_stride;
+    const StateHeader* hdr = reinterpret_cast<const StateHeader*>(blk);
+    const int nf = a.sp.rows[a.cur] * a.sp.cols[a.cur];
+    const bool reset = hdr->nf != nf;
+    // up to four groups per pass: their 12 sums reduce together
+    for (int g0 = 0; g0 < a.G; g0 += 4) {
+      const int ng = min(4, a.G - g0);
+      double acc[12];
+#pragma unroll
+      for (int j = 0; j < 12; ++j) acc[j] = 0.0;
+      for (int i = tid; i < nf; i += kThreads) {
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          if (j < ng) {
+            const int gg = g0 + j;
+            const float* m = reinterpret_cast<const float*>(blk + a.m_off) + (size_t)gg * a.frame_cap;
+            const double sv = a.S[(size_t)(layer * a.G + gg) * a.Lp + a.sp.start[a.cur] + i];
+            const double mv = reset ? 0.0 : (double)m[i];
+            acc[3 * j] += sv * mv;
+            acc[3 * j + 1] += sv * sv;
+            acc[3 * j + 2] += mv * mv;
+          }
+        }
+      }
+#pragma unroll
+      for (int j = 0; j < 12; ++j) acc[j] = wave_sum_d(acc[j]);
+      __syncthreads();
+      if (lane == 0) {
+#pragma unroll
+        for (int j = 0; j < 12; ++j) red12[wave][j] = acc[j];
+      }
+      __syncthreads();
+      if (tid < ng) {   // fixed summation order over the waves
+        double dot = 0.0, ns = 0.0, nm = 0.0;
+        for (int w = 0; w < kWaves; ++w) {
+          dot += red12[w][3 * tid];
+          ns += red12[w][3 * tid + 1];
+          nm += red12[w][3 * tid + 2];
+        }
+        scal[STARKV_SCAL_PHI(a.G) + g0 + tid] =
+            (float)(dot / (sqrt(ns) * sqrt(nm) + (double)a.eps));
+      }
+      // the mean update reads the old m above, so every wave is past its sums
+      __syncthreads();
+      for (int i = tid; i < nf; i += kThreads) {
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          if (j < ng) {
+            const int gg = g0 + j;
+            float* m = reinterpret_cast<float*>(blk + a.m_off) + (size_t)gg * a.frame_cap;
+            const float sv = a.S[(size_t)(layer * a.G + gg) * a.Lp + a.sp.start[a.cur] + i];
+            const float mv = reset ? 0.f : m[i];
+            m[i] = a.rho_t * mv + (1.f - a.rho_t) * sv;
+          }
+        }
+      }
     }
     return;
   }
@@ -398,49 +476,11 @@ __global__ __launch_bounds__(kThreads) void stats_kernel(StatsArgs a) {
     mi = block_sum_d(part, red);
   }
   if (tid == 0) scal[STARKV_SCAL_MI(a.G) + g] = (float)mi;
-
-  // ---- stability of the current frame's row (sec. 3.5)
-  if (a.cur < 0) {
-    if (tid == 0) scal[STARKV_SCAL_PHI(a.G) + g] = 0.f;
-    return;
-  }
-  char* blk = a.state + (size_t)layer * a.state_stride;
-  const StateHeader* hdr = reinterpret_cast<const StateHeader*>(blk);
-  float* m = reinterpret_cast<float*>(blk + a.m_off) + (size_t)g * a.frame_cap;
-  const int nf = a.sp.rows[a.cur] * a.sp.cols[a.cur];
-  const bool reset = hdr->nf != nf;
-  const float* scur = Sg + a.sp.start[a.cur];
-  double dot = 0.0, ns = 0.0, nm = 0.0;
-  for (int i = tid; i < nf; i += kThreads) {
-    const double sv = scur[i];
-    const double mv = reset ? 0.0 : (double)m[i];
-    dot += sv * mv;
-    ns += sv * sv;
-    nm += mv * mv;
-  }
-  dot = block_sum_d(dot, red);
-  ns = block_sum_d(ns, red);
-  nm = block_sum_d(nm, red);
-  const double phi = dot / (sqrt(ns) * sqrt(nm) + (double)a.eps);
-  for (int i = tid; i < nf; i += kThreads) {
-    const float mv = reset ? 0.f : m[i];
-    m[i] = a.rho_t * mv + (1.f - a.rho_t) * scur[i];
-  }
-  if (tid == 0) scal[STARKV_SCAL_PHI(a.G) + g] = (float)phi;
 }
 
-struct FinalArgs {
-  float* scal;
-  char* state;
-  size_t state_stride;
-  int G, sc, nf;      // nf = current frame tokens, or -1
-  float rho_mi, tau, eps, lam, t_min, t_max;
-  int n_warmup, n_ramp;
-};
 
-__global__ __launch_bounds__(64) void finalize_kernel(FinalArgs a) {
-  // one lane per group (G <= 64); wave reductions in a fixed order
-  const int layer = blockIdx.x, lane = threadIdx.x;
+// One wave, one lane per group (G <= 64); wave reductions in a fixed order.
+__device__ void finalize_layer(const FinalArgs& a, int layer, int lane) {
   float* scal = a.scal + (size_t)layer * a.sc;
   char* blk = a.state + (size_t)layer * a.state_stride;
   StateHeader* hdr = reinterpret_cast<StateHeader*>(blk);
@@ -486,6 +526,30 @@ __global__ __launch_bounds__(64) void finalize_kernel(FinalArgs a) {
     hdr->n = n;
     if (a.nf >= 0) hdr->nf = a.nf;
   }
+}
+
+// Every block of a layer counts itself in the layer's state header after
+// its results are out; the last one to arrive runs the layer's finalize and
+// clears the count.  No block waits for another.
+__global__ __launch_bounds__(kThreads) void stats_kernel(StatsArgs a) {
+  __shared__ int last_s;
+  stats_body(a);
+  const int layer = blockIdx.y;
+  StateHeader* hdr = reinterpret_cast<StateHeader*>(a.state + (size_t)layer * a.state_stride);
+  // Thread 0 wrote every value the finalize reads (MI_g or H^); its fence
+  // publishes them before it counts the block.
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    __threadfence();
+    last_s = atomicAdd(&hdr->arrive, 1) == a.G + 1;
+  }
+  __syncthreads();
+  if (!last_s) return;
+  if (threadIdx.x < 64) {
+    __threadfence();          // the other blocks' values
+    finalize_layer(a.fin, layer, threadIdx.x);
+  }
+  if (threadIdx.x == 0) hdr->arrive = 0;
 }
 
 __global__ __launch_bounds__(256) void state_init_kernel(char* state, size_t stride,
@@ -543,8 +607,7 @@ int launch_update_state(const Geometry& g, const starkv_params& p,
                         hipFuncAttributeMaxDynamicSharedMemorySize, (int)kStatsLds);
     configured = true;
   }
-  stats_kernel<<<dim3(g.G + 1, g.n_layers), kThreads, kStatsLds, st>>>(a);
-  FinalArgs f;
+  FinalArgs& f = a.fin;
   f.scal = scalars;
   f.state = a.state;
   f.state_stride = a.state_stride;
@@ -559,7 +622,7 @@ int launch_update_state(const Geometry& g, const starkv_params& p,
   f.t_max = p.t_max;
   f.n_warmup = p.n_warmup;
   f.n_ramp = p.n_ramp;
-  finalize_kernel<<<g.n_layers, 64, 0, st>>>(f);
+  stats_kernel<<<dim3(g.G + 2, g.n_layers), kThreads, kStatsLds, st>>>(a);
   return (int)hipGetLastError();
 }
 
