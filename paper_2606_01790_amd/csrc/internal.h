@@ -27,7 +27,6 @@ struct Geometry {
 
 struct WsLayout {
   size_t part_off;   // float2 [n_layers][G][n_chunks_max][Rpad]  row stats
-  size_t cst_off;    // float  [n_layers][G][Rpad]                merged row stats
   size_t sraw_off;   // float  [n_layers][G][Lp]                  S before pooling
   size_t total;
 };

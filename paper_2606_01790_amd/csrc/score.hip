@@ -77,7 +77,6 @@ int launch_score(const Geometry& g, const starkv_params& p, const void* q,
   a.n_chunks = (g.Lp + chunk - 1) / chunk;
   a.scale = kLog2e / sqrtf((float)g.d);
   a.part = reinterpret_cast<float2*>(static_cast<char*>(ws) + wl.part_off);
-  a.cst = reinterpret_cast<float*>(static_cast<char*>(ws) + wl.cst_off);
   a.sraw = reinterpret_cast<float*>(static_cast<char*>(ws) + wl.sraw_off);
 
   const int err = g.dtype == STARKV_BF16 ? run_score_bf16(a, g.d, g.n_layers, st)

@@ -6,8 +6,9 @@
 // runs in two passes over K:
 //   pass 1  per (layer, group, token chunk): for each window row r, the
 //           chunk's max M_r and sum of 2^(y - M_r), y = q.k * log2(e)/sqrt(d);
-//   pass 2  merges the chunk statistics into c_r = M_r + log2(l_r) and sums
-//           2^(y_rt - c_r) over the group's rows for every token t.
+//   pass 2  merges the chunk statistics into c_r = M_r + log2(l_r) (every
+//           block for its own group) and sums 2^(y_rt - c_r) over the
+//           group's rows for every token t.
 // Both passes run the Q_g x K^T contraction on 32x32 MFMA tiles.  A block
 // has one wave per 32-row block of the group's R = W*H/G window rows; each
 // wave keeps its rows' Q fragments in registers for the whole kernel, and
@@ -29,7 +30,6 @@ struct ScoreArgs {
   int chunk, n_chunks, n_chunks_max;
   float scale;          // log2(e) / sqrt(d)
   float2* part;         // [n_layers][G][n_chunks_max][Rpad]  (M, l)
-  float* cst;           // [n_layers][G][Rpad]  c_r = M_r + log2(l_r)
   float* sraw;          // [n_layers][G][Lp]
 };
 
@@ -240,35 +240,33 @@ __global__ __launch_bounds__(NRB * 64) void score_pass1(ScoreArgs a) {
 }
 
 // ---------------------------------------------------------------- merge
-// c_r = M_r + log2(l_r) from the chunk statistics, fixed merge order; rows
-// past R get +inf so that their 2^(y - c) vanishes in pass 2.
-__global__ __launch_bounds__(512) void score_merge(ScoreArgs a) {
-  const int lg = blockIdx.x;
-  const float2* part = a.part + (size_t)lg * a.n_chunks_max * a.Rpad;
-  for (int r = threadIdx.x; r < a.Rpad; r += blockDim.x) {
-    float Mx = kNegBig, lx = 0.f;
-    for (int c0 = 0; c0 < a.n_chunks; c0 += 8) {
-      float2 p[8];
+// c_r = M_r + log2(l_r) of row r of one (layer, group) from its chunks'
+// statistics, in a fixed merge order; rows past R get +inf so that their
+// 2^(y - c) vanishes in pass 2.
+__device__ inline float merge_row(const ScoreArgs& a, const float2* part, int r) {
+  float Mx = kNegBig, lx = 0.f;
+  for (int c0 = 0; c0 < a.n_chunks; c0 += 8) {
+    float2 p[8];
 #pragma unroll
-      for (int j = 0; j < 8; ++j)   // eight loads in flight
-        p[j] = c0 + j < a.n_chunks ? part[(size_t)(c0 + j) * a.Rpad + r]
-                                   : make_float2(kNegBig, 0.f);
+    for (int j = 0; j < 8; ++j)   // eight loads in flight
+      p[j] = c0 + j < a.n_chunks ? part[(size_t)(c0 + j) * a.Rpad + r]
+                                 : make_float2(kNegBig, 0.f);
 #pragma unroll
-      for (int j = 0; j < 8; ++j) {
-        const float mn = fmaxf(Mx, p[j].x);
-        lx = lx * __builtin_amdgcn_exp2f(Mx - mn) + p[j].y * __builtin_amdgcn_exp2f(p[j].x - mn);
-        Mx = mn;
-      }
+    for (int j = 0; j < 8; ++j) {
+      const float mn = fmaxf(Mx, p[j].x);
+      lx = lx * __builtin_amdgcn_exp2f(Mx - mn) + p[j].y * __builtin_amdgcn_exp2f(p[j].x - mn);
+      Mx = mn;
     }
-    a.cst[(size_t)lg * a.Rpad + r] = (r < a.R) ? Mx + log2f(lx) : INFINITY;
   }
+  return (r < a.R) ? Mx + log2f(lx) : INFINITY;
 }
 
 // ---------------------------------------------------------------- pass 2
 // Query rows on the MFMA M axis: each lane owns one token of the 32-token
 // block and sums 2^(y - c_r) over the 16 rows of the wave's row block it
 // holds (c_r in registers); lane halves and then waves are added in a fixed
-// order through LDS.
+// order through LDS.  Each block first merges its group's chunk statistics
+// into c_r (one row per thread) while its first K tile is in flight.
 template <typename T, int D, int NRB>
 __global__ __launch_bounds__(NRB * 64) void score_pass2(ScoreArgs a) {
   using M = Mfma<T>;
@@ -287,21 +285,25 @@ __global__ __launch_bounds__(NRB * 64) void score_pass2(ScoreArgs a) {
   const int t_end = min(t_begin + a.chunk, a.Lp);
   float* srow = a.sraw + (size_t)(layer * a.G + g) * a.Lp;
 
+  __shared__ __align__(16) float cs[NRB * 32];
+  i32x4 sr[KS::kPerThread];
+  STARKV_STAGE_FETCH(KS, NRB * 64, sr, kg, a.ts, t_begin, a.Lp)
   typename M::frag qf[NK];
   load_q_frags<T, D>(group_q<T, D>(a, layer, g), a.R, wave, qf);
+  {
+    const float2* part = a.part + (size_t)(layer * a.G + g) * a.n_chunks_max * a.Rpad;
+    for (int r = threadIdx.x; r < NRB * 32; r += NRB * 64) cs[r] = merge_row(a, part, r);
+  }
+  STARKV_STAGE_STORE(KS, NRB * 64, sr, kbuf)
+  __syncthreads();
   // c of the rows this lane receives: wave*32 + 8i + 4*half + j
-  const float* cg = a.cst + (size_t)(layer * a.G + g) * a.Rpad + wave * 32 + 4 * half;
   float c[16];
 #pragma unroll
   for (int i = 0; i < 4; ++i) {
-    const f32x4 c4 = *reinterpret_cast<const f32x4*>(cg + 8 * i);
+    const f32x4 c4 = *reinterpret_cast<const f32x4*>(cs + wave * 32 + 4 * half + 8 * i);
 #pragma unroll
     for (int j = 0; j < 4; ++j) c[4 * i + j] = c4[j];
   }
-  i32x4 sr[KS::kPerThread];
-  STARKV_STAGE_FETCH(KS, NRB * 64, sr, kg, a.ts, t_begin, a.Lp)
-  STARKV_STAGE_STORE(KS, NRB * 64, sr, kbuf)
-  __syncthreads();
 
   int buf = 0;
   for (int t0 = t_begin; t0 < t_end; t0 += KS::kRows) {
@@ -342,7 +344,6 @@ int run_passes(const ScoreArgs& a, int n_layers, hipStream_t st) {
   const size_t lds1 = 2 * (size_t)KS::kElems * sizeof(T);
   const size_t lds2 = lds1 + 2 * (size_t)NRB * KS::kRows * sizeof(float);
   score_pass1<T, D, NRB><<<items, NRB * 64, lds1, st>>>(a);
-  score_merge<<<a.G * n_layers, 512, 0, st>>>(a);
   score_pass2<T, D, NRB><<<items, NRB * 64, lds2, st>>>(a);
   return (int)hipGetLastError();
 }

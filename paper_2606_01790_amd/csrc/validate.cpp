@@ -120,8 +120,7 @@ WsLayout ws_layout(const Geometry& g) {
   WsLayout w;
   const size_t lg = (size_t)g.n_layers * g.G;
   w.part_off = 0;
-  w.cst_off = up256(lg * max_chunks(g) * g.Rpad * 2 * sizeof(float));
-  w.sraw_off = w.cst_off + up256(lg * g.Rpad * sizeof(float));
+  w.sraw_off = up256(lg * max_chunks(g) * g.Rpad * 2 * sizeof(float));
   w.total = w.sraw_off + up256(lg * g.Lp * sizeof(float));
   return w;
 }

@@ -76,8 +76,7 @@ def test_sizes():
     chunks = (Lp + 255) // 256
     up = lambda x: (x + 255) // 256 * 256  # noqa: E731
     part = up(28 * 4 * chunks * 224 * 8)    # per-chunk row statistics
-    cst = up(28 * 4 * 224 * 4)              # merged row statistics
-    assert ws == part + cst + up(28 * 4 * Lp * 4)
+    assert ws == part + up(28 * 4 * Lp * 4)
     assert sk.workspace_bytes(dims(G=3)) == 0          # H % G != 0
 
 
