@@ -24,6 +24,7 @@ constexpr int kWaves = kThreads / 64;
 constexpr int kBatch = 8;              // loads in flight per thread
 constexpr int kLdsKeys = 28 * 1024;   // keys cached in LDS (112 KiB)
 constexpr int kCand = 2048;           // keys of the cut's first-digit bucket
+constexpr int kDirect = 256;          // candidates ranked directly, no more digits
 
 struct SelArgs {
   const float* sbar;
@@ -42,7 +43,7 @@ struct SelArgs {
 __global__ __launch_bounds__(kThreads) void select_kernel(SelArgs a) {
   extern __shared__ __align__(16) uint32_t keys[];
   __shared__ int hist[4096];              // first digit; later per-wave digits
-  __shared__ uint32_t cand[kCand];
+  __shared__ __align__(16) uint32_t cand[kCand];
   __shared__ int sp_start[STARKV_MAX_SPANS], sp_end[STARKV_MAX_SPANS];
   __shared__ float sp_dist[STARKV_MAX_SPANS];
   __shared__ int sh_cnt[kWaves];
@@ -176,6 +177,34 @@ __global__ __launch_bounds__(kThreads) void select_kernel(SelArgs a) {
         __syncthreads();
         compact = true;
         n_c = n_cand;
+        if (n_c <= kDirect) {
+          // few candidates: each ranks itself; the one whose rank range holds
+          // the cut's rank is the cut key
+          if (tid < n_c) {
+            const uint32_t key = cand[tid];
+            int less = 0, eq = 0;
+            for (int j0 = 0; j0 < n_c; j0 += 8) {   // 8 keys per trip, 2 reads in flight
+              const i32x4 v0 = *reinterpret_cast<const i32x4*>(cand + j0);
+              const i32x4 v1 = *reinterpret_cast<const i32x4*>(cand + j0 + 4);
+#pragma unroll
+              for (int u = 0; u < 8; ++u) {
+                const uint32_t kj = (uint32_t)(u < 4 ? v0[u] : v1[u - 4]);
+                if (j0 + u < n_c) {
+                  less += kj < key;
+                  eq += kj == key;
+                }
+              }
+            }
+            if (less <= crank && crank < less + eq) {
+              cut_key = key;         // equal keys write equal values
+              cut_rank = crank - less;
+            }
+          }
+          __syncthreads();
+          ck = cut_key;
+          crank = cut_rank;
+          done = 32 - width;   // the cut is exact: no more digits
+        }
       }
     } else {
       for (int i = tid; i < kWaves * 256; i += kThreads) hist[i] = 0;

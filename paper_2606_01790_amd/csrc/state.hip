@@ -61,6 +61,7 @@ constexpr int kBatch = 8;                 // loads in flight per thread
 constexpr int kHistInts = 16384;          // 64 KiB: digit or joint histograms
 constexpr int kKeyCache = 20 * 1024;      // visual keys kept in LDS
 constexpr int kCand = 2048;               // keys in the edges' first-digit buckets
+constexpr int kDirect = 256;              // candidates ranked directly, no more digits
 constexpr size_t kStatsLds =
     (size_t)kHistInts * 4 + (size_t)kKeyCache * 4 + (size_t)kCand * 4;
 
@@ -86,8 +87,11 @@ __device__ void stats_body(const StatsArgs& a) {
   __shared__ uint32_t n_key[64];          // first-digit results
   __shared__ int n_rank[64], n_eq[64];
   __shared__ uint32_t u_hi[64];
-  __shared__ int n_u, n_cand, cand_total;
+  __shared__ int n_u, cand_total;
   __shared__ uint32_t bucket_bits[128];   // first-digit buckets holding an edge
+  __shared__ uint32_t seg_dg[64];         // distinct edge buckets, ascending
+  __shared__ int seg_off[64], seg_cnt[64], seg_cur[64];
+  __shared__ int n_seg;
   __shared__ int nb_s[64];
   __shared__ int nc_s[256];
   __shared__ int sh_cnt[kWaves];
@@ -337,28 +341,37 @@ __device__ void stats_body(const StatsArgs& a) {
           const uint32_t dg = (n_key[tid] >> shift) & (uint32_t)(nb - 1);
           atomicOr(&bucket_bits[dg >> 5], 1u << (dg & 31));
         }
-        if (wave == 0) {   // keys in the edges' buckets (distinct buckets once)
+        if (wave == 0) {   // keys in the edges' buckets: one segment per bucket
           const bool on = lane < n_t;
           const uint32_t dg = on ? ((n_key[lane] >> shift) & (uint32_t)(nb - 1)) : 0u;
           const uint32_t dp = (uint32_t)__shfl_up((int)dg, 1);
           const bool fresh = on && (lane == 0 || dp != dg);
-          int v = fresh ? n_eq[lane] : 0;
-#pragma unroll
-          for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o);
-          if (lane == 0) { cand_total = v; n_cand = 0; }
+          const int cnt = fresh ? n_eq[lane] : 0;
+          const int inc = wave_incl_scan(cnt);
+          const int slot = wave_incl_scan(fresh ? 1 : 0) - 1;
+          if (fresh) {
+            seg_dg[slot] = dg;
+            seg_off[slot] = inc - cnt;
+            seg_cnt[slot] = cnt;
+            seg_cur[slot] = 0;
+          }
+          if (lane == 63) { cand_total = inc; n_seg = slot + 1; }
         }
         __syncthreads();
         if (done + width < 32 && cand_total <= kCand) {
-          // compact them (order is irrelevant for counting)
+          // compact them, each bucket's keys in its own segment (in any
+          // order inside it)
+          const int ns = n_seg;
           auto keep = [&](uint32_t key, bool valid) {
             const uint32_t dg = (key >> shift) & (uint32_t)(nb - 1);
-            const bool m = valid && ((bucket_bits[dg >> 5] >> (dg & 31)) & 1u);
-            const uint64_t bal = __ballot(m);
-            int base = 0;
-            if (lane == 0 && bal) base = atomicAdd(&n_cand, __popcll(bal));
-            base = __shfl(base, 0);
-            const uint64_t below = lane == 0 ? 0ull : (~0ull >> (64 - lane));
-            if (m) cand[base + __popcll(bal & below)] = key;
+            if (valid && ((bucket_bits[dg >> 5] >> (dg & 31)) & 1u)) {
+              int lo = 0, hi = ns - 1;
+              while (lo < hi) {
+                const int mid = (lo + hi) >> 1;
+                if (seg_dg[mid] < dg) lo = mid + 1; else hi = mid;
+              }
+              cand[seg_off[lo] + atomicAdd(&seg_cur[lo], 1)] = key;
+            }
           };
           if (cached) {
             for (int i0 = 0; i0 < N; i0 += kThreads) {
@@ -377,7 +390,45 @@ __device__ void stats_body(const StatsArgs& a) {
           }
           __syncthreads();
           compact = true;
-          n_c = n_cand;
+          n_c = cand_total;
+          if (n_c <= kDirect) {
+            // few candidates: each ranks itself among its bucket's keys; the
+            // one whose rank range holds an edge's rank is that edge's key
+            if (tid < n_c) {
+              const uint32_t key = cand[tid];
+              const uint32_t pre = key_hi(key, shift);
+              int sg = 0;
+              while (sg + 1 < ns && seg_off[sg + 1] <= tid) ++sg;
+              const int j_end = seg_off[sg] + seg_cnt[sg];
+              int less = 0, eq = 0;
+              for (int j0 = seg_off[sg]; j0 < j_end; j0 += 4) {
+                uint32_t kv[4];
+#pragma unroll
+                for (int u = 0; u < 4; ++u) kv[u] = cand[min(j0 + u, j_end - 1)];
+#pragma unroll
+                for (int u = 0; u < 4; ++u) {
+                  const bool in = j0 + u < j_end;
+                  less += in && kv[u] < key;
+                  eq += in && kv[u] == key;
+                }
+              }
+              for (int b = 0; b < n_t; ++b) {
+                const int r = t_rank[b];
+                if (key_hi(t_key[b], shift) == pre && less <= r && r < less + eq) {
+                  n_key[b] = key;      // equal keys write equal values
+                  n_rank[b] = r - less;
+                  n_eq[b] = eq;
+                }
+              }
+            }
+            __syncthreads();
+            if (tid < n_t) {
+              t_key[tid] = n_key[tid];
+              t_rank[tid] = n_rank[tid];
+              t_eq[tid] = n_eq[tid];
+            }
+            done = 32 - width;   // every edge is exact: no more digits
+          }
         }
       } else {
         for (int b = wave; b < n_t; b += kWaves) {
