@@ -122,6 +122,59 @@ def test_config4_budget_sweep_sampled_layers():
     run_trajectory(4, layers=[0, 13])
 
 
+def oracle_state_from_gpu(state_bytes_np, layer, G, frame_cap):
+    """The oracle's LayerState equal to one layer's GPU state block: a 64-byte
+    header (int32 magic, G, frame_cap, n, nf, ...), MI_bar[G] float32 padded
+    to 16 bytes, then m[G][frame_cap] float32; blocks padded to 256 bytes."""
+    m_off = 64 + (G * 4 + 15) // 16 * 16
+    stride = (m_off + G * frame_cap * 4 + 255) // 256 * 256
+    blk = state_bytes_np[layer * stride:(layer + 1) * stride]
+    hdr = blk[:64].view(np.int32)
+    n, nf = int(hdr[3]), int(hdr[4])
+    mi_bar = blk[64:64 + 4 * G].view(np.float32).astype(np.float64)
+    m = blk[m_off:m_off + 4 * G * frame_cap].view(np.float32).reshape(G, frame_cap)
+    return O.LayerState(G, mi_bar, m[:, :nf].astype(np.float64), n)
+
+
+def test_config5_long_trajectory_sampled_steps():
+    """The 30-step 2560x1440 trajectory (W = 64: 448 window rows per group,
+    up to 140K past tokens, keys beyond every LDS cache) for layers 0 and 27
+    on the GPU.  At steps 1, 2, 16 and 30 the oracle runs that step from the
+    GPU's own state after the previous step, and every output is compared."""
+    spec = WL.SPECS[5]
+    p = params_for(5)
+    op = oracle_params(p)
+    layers = [0, 27]
+    host = HostFrames(spec)
+    frame_cap = spec.n_frame
+    case = ArrayCase(spec.H, spec.G, spec.d, spec.W, len(layers), spec.L(spec.steps),
+                     spec.dtype, p, frame_cap)
+    report = {}
+    for step in range(1, spec.steps + 1):
+        L, spans, B = spec.L(step), spec.spans(step), spec.budgets(step)[0]
+        caches = [host.cache(layer, step) for layer in layers]
+        Ks = np.stack([c[0] for c in caches])
+        Vs = np.stack([c[1] for c in caches])
+        Qs = np.stack([host.tr.window_q(layer, step) for layer in layers])
+        check = step in (1, 2, 16, 30)
+        if check:
+            prev = case.state.cpu().numpy()
+        say(f"cfg5 step {step}: L={L} B={B}{' (checked)' if check else ''}")
+        gpu = case.run(Qs, Ks, Vs, L, spans, step, B)
+        if not check:
+            continue
+        for i, layer in enumerate(layers):
+            st = oracle_state_from_gpu(prev, i, spec.G, frame_cap)
+            out, _ = O.compress_layer(WL.to_float64(Qs[i], spec.dtype),
+                                      WL.to_float64(Ks[i], spec.dtype), None, L, spec.W,
+                                      spans, step, B, op, st, copy_rows=(Ks[i], Vs[i]))
+            g = {k: v[i] for k, v in gpu.items()}
+            check_layer(f"cfg5 step{step} L{layer}", Ks[i], Vs[i], L, spec.W, spans, step,
+                        B, op, spec.G, g, out, report)
+    say(f"cfg5 done: max S rel {max(report['S']):.2e}, idx band tokens "
+        f"{sum(report['idx_band'])}")
+
+
 def test_determinism_bitwise():
     spec = WL.SPECS[2]
     p = params_for(2, prior_active=True)
