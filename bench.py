@@ -42,6 +42,9 @@ def parse():
                     help="oracle time of the CPU sample: layers are added, each with its "
                          "whole trajectory, until this much oracle time has run")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--groups", type=int, default=1,
+                    help="layer groups per step, each on its own HIP stream (1: one "
+                         "launch of every call for all layers)")
     ap.add_argument("--eager", action="store_true",
                     help="launch every call from Python instead of replaying a HIP graph")
     ap.add_argument("--copy-calibration", action="store_true",
@@ -119,9 +122,24 @@ class Workload:
         sp = self.spec
         return self.sk.make_dims(sp.n_layers, sp.H, sp.G, sp.d, sp.L(s), sp.W, self.dt)
 
-    def trajectory(self, state):
-        """The hot path over the whole trajectory: the four calls per step."""
+    def trajectory(self, state, groups=1):
+        """The hot path over the whole trajectory: the four calls per step, for
+        all layers at once or as `groups` layer groups on as many streams."""
         sk, sp, p = self.sk, self.spec, self.params
+        if groups > 1:
+            from paper_2606_01790_amd.pipeline import LayerGroups
+            if getattr(self, "_lg", None) is None or len(self._lg.ranges) != groups:
+                self._lg = LayerGroups(sp.n_layers, groups, self.ws.numel(), self.ws.device)
+            d1 = sk.make_dims(1, sp.H, sp.G, sp.d, sp.L(sp.steps), sp.W, self.dt)
+            stride = sk.state_bytes(d1, self.frame_cap)
+            for s in range(1, sp.steps + 1):
+                i = s - 1
+                self._lg.run(
+                    lambda n, s=s: sk.make_dims(n, sp.H, sp.G, sp.d, sp.L(s), sp.W, self.dt),
+                    p, s, sp.spans(s), sp.budgets(s)[0], self.Q[i], self.K[i], self.V[i],
+                    self.S, self.sbar, self.gstar, self.s, self.idx, self.k_out, self.v_out,
+                    self.scal, self.nscal, state, stride, self.frame_cap)
+            return
         for s in range(1, sp.steps + 1):
             i = s - 1
             dims = self.dims(s)
@@ -222,13 +240,13 @@ def main():
     log(f"warmup {args.warmup}")
     k = 0
     for _ in range(args.warmup):
-        wl.trajectory(wl.states[k])
+        wl.trajectory(wl.states[k], args.groups)
         k += 1
     torch.cuda.synchronize()
 
     stream = torch.cuda.current_stream()
     if args.eager:
-        run = lambda: wl.trajectory(wl.states[0])  # noqa: E731
+        run = lambda: wl.trajectory(wl.states[0], args.groups)  # noqa: E731
     else:
         # One trajectory (a fresh state, then every step's four calls) captured
         # into a HIP graph: the timed region replays it, so the host's Python
@@ -238,7 +256,7 @@ def main():
         g = torch.cuda.CUDAGraph()
         with torch.cuda.graph(g):
             sk.state_init(dmax, graph_state, wl.frame_cap)
-            wl.trajectory(graph_state)
+            wl.trajectory(graph_state, args.groups)
         torch.cuda.synchronize()
         run = g.replay
         for _ in range(args.warmup):
@@ -299,7 +317,9 @@ def main():
                    "trajectory_steps": spec.steps, "budget_pct": list(spec.pcts),
                    "layer_tokens_per_step": layer_tokens,
                    "bytes_alg_per_step": bytes_alg,
-                   "launch": "eager" if args.eager else "hipgraph"},
+                   "launch": ("eager" if args.eager else "hipgraph")
+                   + (f", {args.groups} layer groups on {args.groups} streams"
+                      if args.groups > 1 else "")},
         "hbm_frac_path": round(bytes_alg / (ms_per_step * 1e-3) / (HBM_PEAK_GBS * 1e9), 4),
         "per_call_us": per_call_us,
         "roofline": roofline,

@@ -25,6 +25,59 @@ def to_device(arr: np.ndarray, dtype: str, device) -> torch.Tensor:
     return t.to(device, non_blocking=False)
 
 
+class LayerGroups:
+    """The four calls of one step run as `n` contiguous layer groups on `n`
+    HIP streams.  Group j's scoring starts when group j-1's scoring has
+    finished, so the statistics, selection and gather of one group (few
+    workgroups, latency-bound) overlap the scoring of the next; the caller's
+    stream waits for every group at the end of the step.
+
+    Each layer's slice of every buffer is contiguous, so a group's arguments
+    are pointer offsets into the full tensors; every group has its own
+    workspace.  Group 0 runs on the caller's current stream."""
+
+    def __init__(self, n_layers: int, n_groups: int, ws_bytes: int, device):
+        n_groups = max(1, min(n_groups, n_layers))
+        b = [(i * n_layers) // n_groups for i in range(n_groups + 1)]
+        self.ranges = [(b[i], b[i + 1]) for i in range(n_groups)]
+        self.ws = [torch.zeros(max(ws_bytes, 16), dtype=torch.uint8, device=device)
+                   for _ in self.ranges]
+        self.streams = [None] + [torch.cuda.Stream(device=device)
+                                 for _ in self.ranges[1:]]
+
+    def run(self, make_dims, params, step, spans, B, Q, K, V, S, sbar, gstar, s, idx,
+            k_out, v_out, scal, nscal, state, state_stride, frame_cap):
+        """make_dims(n_layers) -> dims of this step for that many layers."""
+        cur = torch.cuda.current_stream()
+        prev_scored = None
+        for j, (l0, l1) in enumerate(self.ranges):
+            st = cur if j == 0 else self.streams[j]
+            if prev_scored is not None:
+                st.wait_event(prev_scored)
+            dims = make_dims(l1 - l0)
+            G, Lp, W, d = dims.G, dims.L - dims.W, dims.W, dims.d
+            kg, vg = K[l0:l1], V[l0:l1]
+            lay = sk.contiguous_layout(kg, dims)
+            n_out = G * (B + W) * d
+            Sg = S[l0 * G * Lp:l1 * G * Lp]
+            sb = sbar[l0 * Lp:l1 * Lp]
+            gs = gstar[l0 * Lp:l1 * Lp]
+            scg = scal[l0 * nscal:l1 * nscal]
+            stg = state[l0 * state_stride:l1 * state_stride]
+            ws = self.ws[j]
+            sk.score(dims, params, Q[l0:l1], kg, lay, Sg, sb, gs, ws, st)
+            if j + 1 < len(self.ranges):
+                prev_scored = torch.cuda.Event()
+                prev_scored.record(st)
+            sk.update_state(dims, params, Sg, sb, spans, step, stg, frame_cap, scg, ws, st)
+            sk.select(dims, params, sb, gs, scg, spans, step, B, s[l0 * Lp:l1 * Lp],
+                      idx[l0 * B:l1 * B] if B else idx, ws, st)
+            sk.compact(dims, kg, vg, lay, idx[l0 * B:l1 * B] if B else idx, B,
+                       k_out[l0 * n_out:l1 * n_out], v_out[l0 * n_out:l1 * n_out], st)
+        for st in self.streams[1:]:
+            cur.wait_stream(st)
+
+
 class TrajectoryRunner:
     """Holds every device buffer of a trajectory of `spec` and runs its steps."""
 
@@ -107,10 +160,23 @@ class TrajectoryRunner:
         sk.compact(dims, self.K, self.V, self.layout, self.idx, B, self.k_out,
                    self.v_out, stream)
 
-    def run_step(self, step: int, B: int, stream=None):
-        """The compression stage of one step for all layers: the four calls."""
-        self.score_and_update(step, stream)
-        self.select_and_compact(step, B, stream)
+    def run_step(self, step: int, B: int, stream=None, groups: int = 1):
+        """The compression stage of one step for all layers: the four calls,
+        on the current stream, or as `groups` layer groups on as many streams
+        (see LayerGroups)."""
+        if groups <= 1:
+            self.score_and_update(step, stream)
+            self.select_and_compact(step, B, stream)
+            return
+        sp = self.spec
+        if getattr(self, "_groups", None) is None or len(self._groups.ranges) != groups:
+            self._groups = LayerGroups(sp.n_layers, groups, self.ws.numel(), self.device)
+        d1 = sk.make_dims(1, sp.H, sp.G, sp.d, sp.L(sp.steps), sp.W, self.dt)
+        self._groups.run(
+            lambda n: sk.make_dims(n, sp.H, sp.G, sp.d, sp.L(step), sp.W, self.dt),
+            self.params, step, sp.spans(step), B, self.Q, self.K, self.V, self.S,
+            self.sbar, self.gstar, self.s, self.idx, self.k_out, self.v_out, self.scal,
+            self.nscal, self.state, sk.state_bytes(d1, self.frame_cap), self.frame_cap)
 
     # ---- views of the outputs of the last step (host copies)
     def outputs(self, step: int, B: int) -> dict:

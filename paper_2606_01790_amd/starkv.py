@@ -152,8 +152,10 @@ def contiguous_layout(t, dims: Dims) -> KVLayout:
 
 
 def _stream(stream):
+    """A hipStream_t handle: a torch stream, a raw handle, or None for the
+    current torch stream."""
     if stream is not None:
-        return c_void_p(stream)
+        return c_void_p(getattr(stream, "cuda_stream", stream))
     import torch
     return c_void_p(torch.cuda.current_stream().cuda_stream)
 

@@ -51,7 +51,7 @@ class HostFrames:
         return np.concatenate(ks + [k], axis=1), np.concatenate(vs + [v], axis=1)
 
 
-def run_trajectory(cid, layers=None, prior_active=False, steps=None):
+def run_trajectory(cid, layers=None, prior_active=False, steps=None, groups=1):
     spec = WL.SPECS[cid]
     p = params_for(cid, prior_active)
     op = oracle_params(p)
@@ -65,7 +65,11 @@ def run_trajectory(cid, layers=None, prior_active=False, steps=None):
     for step in range(1, (steps or spec.steps) + 1):
         say(f"cfg{cid} step {step}: load + score/update")
         runner.load_step(step)
-        runner.score_and_update(step)
+        if groups > 1:              # the bench's launch: layer groups on streams
+            assert len(spec.budgets(step)) == 1
+            runner.run_step(step, spec.budgets(step)[0], groups=groups)
+        else:
+            runner.score_and_update(step)
         L, W = spec.L(step), spec.W
         spans = spec.spans(step)
         budgets = spec.budgets(step)
@@ -79,7 +83,8 @@ def run_trajectory(cid, layers=None, prior_active=False, steps=None):
             orc_base[layer] = (out, K, V)
         for B in budgets:
             say(f"cfg{cid} step {step} B={B}: select/compact")
-            runner.select_and_compact(step, B)
+            if groups <= 1:
+                runner.select_and_compact(step, B)
             torch.cuda.synchronize()
             gpu = runner.outputs(step, B)
             for layer in layers:
@@ -114,6 +119,13 @@ def test_config3_28_layers_5_steps():
 
 def test_config3_prior_active_sampled_layers():
     run_trajectory(3, layers=[0, 1, 2, 3, 27], prior_active=True)
+
+
+def test_config3_layer_groups_on_two_streams():
+    """The bench's launch configuration: each step as two layer groups on two
+    HIP streams (the second group's scoring overlaps the first group's
+    statistics, selection and gather); layers at both group edges."""
+    run_trajectory(3, layers=[0, 13, 14, 27], prior_active=True, groups=2)
 
 
 def test_config4_budget_sweep_sampled_layers():
