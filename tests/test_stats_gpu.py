@@ -143,3 +143,30 @@ def test_many_bins_fine_grid():
     p.n_bins, p.grid = 64, 16
     sbar = rng.uniform(1e-4, 1e-2, Lp).astype(np.float32)
     run_stats("K64 M16", [S], sbar, spans, 3, p)
+
+
+@pytest.mark.parametrize("rows,cols,K,M", [(1, 1, 8, 8), (1, 2, 8, 8), (1, 7, 8, 8),
+                                            (3, 3, 8, 8), (4, 5, 1, 8), (6, 7, 8, 1),
+                                            (9, 11, 64, 16)])
+def test_tiny_frames_and_degenerate_bins(rows, cols, K, M):
+    """Fewer visual tokens than bins (empty bins, coinciding edges), a single
+    bin, a 1x1 grid: the edge selection's small-candidate path."""
+    rng = np.random.default_rng(rows * 100 + cols)
+    spans, Lp = layout(3, rows, cols, gap=5, head=3, tail=40)
+    S = rng.lognormal(-7, 1.0, (1, 2, Lp)).astype(np.float32)
+    p = sk.params_default()
+    p.n_bins, p.grid = K, M
+    sbar = rng.uniform(1e-4, 1e-2, Lp).astype(np.float32)
+    run_stats(f"tiny {rows}x{cols} K{K} M{M}", [S, S[:, ::-1].copy()], sbar, spans, 3, p)
+
+
+def test_all_scores_equal_and_two_levels():
+    """Every visual key equal (no radix digit at all), and two levels with
+    the edges inside the runs of equal keys."""
+    spans, Lp = layout(4, 20, 30)
+    S = np.empty((1, 2, Lp), np.float32)
+    S[0, 0] = 3e-3
+    rng = np.random.default_rng(5)
+    S[0, 1] = np.where(rng.random(Lp) < 0.3, 1e-3, 4e-3).astype(np.float32)
+    sbar = np.full(Lp, 1e-3, np.float32)
+    run_stats("equal keys", [S, S], sbar, spans, 4, sk.params_default())
