@@ -102,25 +102,20 @@ struct KStage {
   static constexpr int kVecs = kRows * kVecPerRow;
   static constexpr int kPerThread = (kVecs + NTHREADS - 1) / NTHREADS;
   static constexpr int kElems = kRows * kStride;
+  // Thread t stages vectors t + j*NTHREADS: the same 16-byte column of rows
+  // t/kVecPerRow + j*kRowStep, since NTHREADS is a multiple of kVecPerRow.
+  static_assert(NTHREADS % kVecPerRow == 0, "row-aligned staging");
+  static constexpr int kRowStep = NTHREADS / kVecPerRow;
+  // vector j may fall past the tile's last row (then it repeats that row)
+  static constexpr bool may_pass(int j) { return (kRowStep - 1) + j * kRowStep >= kRows; }
 };
 
 // Tile staging, written inline in each kernel over a local array so that the
-// staging vectors stay in registers.  Threads past the tile's vector count
-// repeat its last vector (every load and store is unconditional).
-#define STARKV_STAGE_FETCH(KS, NTH, r, kg, ts, t0, Lp)                           \
-  _Pragma("unroll") for (int j_ = 0; j_ < KS::kPerThread; ++j_) {                \
-    const int v_ = min((int)threadIdx.x + j_ * (NTH), KS::kVecs - 1);            \
-    const int row_ = v_ / KS::kVecPerRow, part_ = v_ % KS::kVecPerRow;           \
-    const int tok_ = min((t0) + row_, (Lp) - 1);                                 \
-    r[j_] = *reinterpret_cast<const i32x4*>((kg) + (int64_t)tok_ * (ts) +        \
-                                            part_ * KS::kElemPerVec);            \
-  }
-#define STARKV_STAGE_STORE(KS, NTH, r, buf)                                      \
-  _Pragma("unroll") for (int j_ = 0; j_ < KS::kPerThread; ++j_) {                \
-    const int v_ = min((int)threadIdx.x + j_ * (NTH), KS::kVecs - 1);            \
-    const int row_ = v_ / KS::kVecPerRow, part_ = v_ % KS::kVecPerRow;           \
-    *reinterpret_cast<i32x4*>((buf) + row_ * KS::kStride + part_ * KS::kElemPerVec) = r[j_]; \
-  }
+// staging vectors stay in registers; every load and store is unconditional.
+// `full`: the tile's rows all lie before Lp, so no token index is clamped and
+// the addresses step by a uniform stride.
+#define STARKV_STAGE_FETCH(KS, NTH, r, kg, ts, t0, Lp, full)                       {                                                                                  const int r0_ = (int)threadIdx.x / KS::kVecPerRow;                               const int c0_ = ((int)threadIdx.x % KS::kVecPerRow) * KS::kElemPerVec;           if (full) {                                                                        const auto* p_ = (kg) + (int64_t)((t0) + r0_) * (ts) + c0_;                      _Pragma("unroll") for (int j_ = 0; j_ < KS::kPerThread; ++j_) {                    if (KS::may_pass(j_)) {                                                            const int row_ = min(r0_ + j_ * KS::kRowStep, KS::kRows - 1);                    r[j_] = *reinterpret_cast<const i32x4*>((kg) + (int64_t)((t0) + row_) * (ts) + c0_);         } else {                                                                           r[j_] = *reinterpret_cast<const i32x4*>(p_ + (int64_t)(j_ * KS::kRowStep) * (ts));         }                                                                              }                                                                              } else {                                                                           _Pragma("unroll") for (int j_ = 0; j_ < KS::kPerThread; ++j_) {                    const int row_ = min(r0_ + j_ * KS::kRowStep, KS::kRows - 1);                    const int tok_ = min((t0) + row_, (Lp) - 1);                                     r[j_] = *reinterpret_cast<const i32x4*>((kg) + (int64_t)tok_ * (ts) + c0_);       }                                                                              }                                                                              }
+#define STARKV_STAGE_STORE(KS, NTH, r, buf)                                        {                                                                                  const int r0_ = (int)threadIdx.x / KS::kVecPerRow;                               const int c0_ = ((int)threadIdx.x % KS::kVecPerRow) * KS::kElemPerVec;           auto* q_ = (buf) + r0_ * KS::kStride + c0_;                                      _Pragma("unroll") for (int j_ = 0; j_ < KS::kPerThread; ++j_) {                    if (KS::may_pass(j_)) {                                                            const int row_ = min(r0_ + j_ * KS::kRowStep, KS::kRows - 1);                    *reinterpret_cast<i32x4*>((buf) + row_ * KS::kStride + c0_) = r[j_];           } else {                                                                           *reinterpret_cast<i32x4*>(q_ + j_ * KS::kRowStep * KS::kStride) = r[j_];       }                                                                              }                                                                              }
 
 // Q fragments of the 32 window rows a wave owns (row block `wave` of the
 // group), held in registers for the whole kernel; rows past R are zero.
@@ -162,7 +157,7 @@ __global__ __launch_bounds__(NRB * 64) void score_pass1(ScoreArgs a) {
   typename M::frag qf[NK];
   load_q_frags<T, D>(group_q<T, D>(a, layer, g), a.R, wave, qf);
   i32x4 sr[KS::kPerThread];
-  STARKV_STAGE_FETCH(KS, NRB * 64, sr, kg, a.ts, t_begin, a.Lp)
+  STARKV_STAGE_FETCH(KS, NRB * 64, sr, kg, a.ts, t_begin, a.Lp, t_begin + KS::kRows <= a.Lp)
   STARKV_STAGE_STORE(KS, NRB * 64, sr, kbuf)
   __syncthreads();
 
@@ -202,7 +197,7 @@ __global__ __launch_bounds__(NRB * 64) void score_pass1(ScoreArgs a) {
   int buf = 0;
   for (int t0 = t_begin; t0 < t_end; t0 += KS::kRows) {
     const bool more = t0 + KS::kRows < t_end;
-    if (more) { STARKV_STAGE_FETCH(KS, NRB * 64, sr, kg, a.ts, t0 + KS::kRows, a.Lp) }
+    if (more) { STARKV_STAGE_FETCH(KS, NRB * 64, sr, kg, a.ts, t0 + KS::kRows, a.Lp, t0 + 2 * KS::kRows <= a.Lp) }
     const T* tile = kbuf + buf * KS::kElems;
     if (t0 + KS::kRows <= t_end) {
       // full tile: branch-free, the MFMA chain of block b+1 is issued before
@@ -287,7 +282,7 @@ __global__ __launch_bounds__(NRB * 64) void score_pass2(ScoreArgs a) {
 
   __shared__ __align__(16) float cs[NRB * 32];
   i32x4 sr[KS::kPerThread];
-  STARKV_STAGE_FETCH(KS, NRB * 64, sr, kg, a.ts, t_begin, a.Lp)
+  STARKV_STAGE_FETCH(KS, NRB * 64, sr, kg, a.ts, t_begin, a.Lp, t_begin + KS::kRows <= a.Lp)
   typename M::frag qf[NK];
   load_q_frags<T, D>(group_q<T, D>(a, layer, g), a.R, wave, qf);
   {
@@ -308,7 +303,7 @@ __global__ __launch_bounds__(NRB * 64) void score_pass2(ScoreArgs a) {
   int buf = 0;
   for (int t0 = t_begin; t0 < t_end; t0 += KS::kRows) {
     const bool more = t0 + KS::kRows < t_end;
-    if (more) { STARKV_STAGE_FETCH(KS, NRB * 64, sr, kg, a.ts, t0 + KS::kRows, a.Lp) }
+    if (more) { STARKV_STAGE_FETCH(KS, NRB * 64, sr, kg, a.ts, t0 + KS::kRows, a.Lp, t0 + 2 * KS::kRows <= a.Lp) }
     const T* tile = kbuf + buf * KS::kElems;
     float* rs = red + buf * (NRB * KS::kRows);
 #pragma unroll
