@@ -92,6 +92,7 @@ __device__ void stats_body(const StatsArgs& a) {
   __shared__ uint32_t seg_dg[64];         // distinct edge buckets, ascending
   __shared__ int seg_off[64], seg_cnt[64], seg_cur[64];
   __shared__ int n_seg;
+  __shared__ uint32_t cand_v[kDirect];    // fused pass: cell << 24 | visual index
   __shared__ int nb_s[64];
   __shared__ int nc_s[256];
   __shared__ int sh_cnt[kWaves];
@@ -265,8 +266,48 @@ __device__ void stats_body(const StatsArgs& a) {
     // histogram per distinct prefix.  After the first digit the keys in the
     // edges' buckets are compacted into LDS when they fit, and the later
     // digits scan only those.
-    bool first = true, compact = false;
-    int n_c = 0;
+    bool first = true, compact = false, fused = false;
+    int n_c = 0, f_shift = 0, f_nb = 1;
+    // Few candidates, compacted into one segment per edge bucket: each ranks
+    // itself among its bucket's keys; the one whose rank range holds an
+    // edge's rank is that edge's key.  Leaves the exact edges in t_*.
+    auto direct_rank = [&](int shift) {
+      const int ns = n_seg;
+      if (tid < n_c) {
+        const uint32_t key = cand[tid];
+        const uint32_t pre = key_hi(key, shift);
+        int sg = 0;
+        while (sg + 1 < ns && seg_off[sg + 1] <= tid) ++sg;
+        const int j_end = seg_off[sg] + seg_cnt[sg];
+        int less = 0, eq = 0;
+        for (int j0 = seg_off[sg]; j0 < j_end; j0 += 4) {
+          uint32_t kv[4];
+#pragma unroll
+          for (int u = 0; u < 4; ++u) kv[u] = cand[min(j0 + u, j_end - 1)];
+#pragma unroll
+          for (int u = 0; u < 4; ++u) {
+            const bool in = j0 + u < j_end;
+            less += in && kv[u] < key;
+            eq += in && kv[u] == key;
+          }
+        }
+        for (int b = 0; b < n_t; ++b) {
+          const int r = t_rank[b];
+          if (key_hi(t_key[b], shift) == pre && less <= r && r < less + eq) {
+            n_key[b] = key;      // equal keys write equal values
+            n_rank[b] = r - less;
+            n_eq[b] = eq;
+          }
+        }
+      }
+      __syncthreads();
+      if (tid < n_t) {
+        t_key[tid] = n_key[tid];
+        t_rank[tid] = n_rank[tid];
+        t_eq[tid] = n_eq[tid];
+      }
+      __syncthreads();
+    };
     for (int done = common; done < 32;) {
       const int width = min(first ? 12 : 8, 32 - done);
       const int shift = 32 - done - width;
@@ -358,7 +399,16 @@ __device__ void stats_body(const StatsArgs& a) {
           if (lane == 63) { cand_total = inc; n_seg = slot + 1; }
         }
         __syncthreads();
-        if (done + width < 32 && cand_total <= kCand) {
+        if (cand_total <= kDirect && K * M * M <= kHistInts && N < (1 << 24)) {
+          // few keys share the edges' buckets: the joint histogram pass
+          // below also collects them, and they are binned once the edges
+          // are exact
+          fused = true;
+          f_shift = shift;
+          f_nb = nb;
+          n_c = cand_total;
+          done = 32 - width;
+        } else if (done + width < 32 && cand_total <= kCand) {
           // compact them, each bucket's keys in its own segment (in any
           // order inside it)
           const int ns = n_seg;
@@ -392,41 +442,7 @@ __device__ void stats_body(const StatsArgs& a) {
           compact = true;
           n_c = cand_total;
           if (n_c <= kDirect) {
-            // few candidates: each ranks itself among its bucket's keys; the
-            // one whose rank range holds an edge's rank is that edge's key
-            if (tid < n_c) {
-              const uint32_t key = cand[tid];
-              const uint32_t pre = key_hi(key, shift);
-              int sg = 0;
-              while (sg + 1 < ns && seg_off[sg + 1] <= tid) ++sg;
-              const int j_end = seg_off[sg] + seg_cnt[sg];
-              int less = 0, eq = 0;
-              for (int j0 = seg_off[sg]; j0 < j_end; j0 += 4) {
-                uint32_t kv[4];
-#pragma unroll
-                for (int u = 0; u < 4; ++u) kv[u] = cand[min(j0 + u, j_end - 1)];
-#pragma unroll
-                for (int u = 0; u < 4; ++u) {
-                  const bool in = j0 + u < j_end;
-                  less += in && kv[u] < key;
-                  eq += in && kv[u] == key;
-                }
-              }
-              for (int b = 0; b < n_t; ++b) {
-                const int r = t_rank[b];
-                if (key_hi(t_key[b], shift) == pre && less <= r && r < less + eq) {
-                  n_key[b] = key;      // equal keys write equal values
-                  n_rank[b] = r - less;
-                  n_eq[b] = eq;
-                }
-              }
-            }
-            __syncthreads();
-            if (tid < n_t) {
-              t_key[tid] = n_key[tid];
-              t_rank[tid] = n_rank[tid];
-              t_eq[tid] = n_eq[tid];
-            }
+            direct_rank(shift);
             done = 32 - width;   // every edge is exact: no more digits
           }
         }
@@ -446,9 +462,93 @@ __device__ void stats_body(const StatsArgs& a) {
       first = false;
     }
 
+    const int ncell = M * M;
+    if (fused) {
+      // ---- joint histogram of the tokens outside the edges' buckets (their
+      // bin is the count of edges in lower buckets); the others are kept
+      // with their visual index
+      for (int i = tid; i < K * ncell; i += kThreads) hist[i] = 0;
+      uint32_t eb[8];
+#pragma unroll
+      for (int j = 0; j < 8; ++j)
+        eb[j] = j < n_t ? ((t_key[j] >> f_shift) & (uint32_t)(f_nb - 1)) : 0xFFFFFFFFu;
+      auto lower_edges = [&](uint32_t d) {
+        int n = 0;
+        if (n_t <= 8) {
+#pragma unroll
+          for (int j = 0; j < 8; ++j) n += eb[j] < d;
+        } else {
+          for (int b = 0; b < n_t; ++b) n += ((t_key[b] >> f_shift) & (uint32_t)(f_nb - 1)) < d;
+        }
+        return n;
+      };
+      __syncthreads();
+      const int ns = n_seg;
+      for (int s = 0; s < a.sp.n; ++s) {
+        const int rows = a.sp.rows[s], cols = a.sp.cols[s];
+        const int n_s = rows * cols;
+        const uint32_t* kcs = kc + a.sp.off[s];
+        const float* src = Sg + a.sp.start[s];
+        const float fr = (float)M / (float)rows, fc = (float)M / (float)cols;
+        int r = tid / cols, c = tid - (tid / cols) * cols;
+        const int dq = kThreads / cols, dr = kThreads - dq * cols;
+        for (int i0 = 0; i0 < n_s; i0 += kThreads) {
+          const int i = i0 + tid;
+          if (i < n_s) {
+            const uint32_t key = cached ? kcs[i] : fkey(src[i]);
+            const uint32_t d = (key >> f_shift) & (uint32_t)(f_nb - 1);
+            const int cell = scaled_index(r, M, rows, fr) * M + scaled_index(c, M, cols, fc);
+            if ((bucket_bits[d >> 5] >> (d & 31)) & 1u) {
+              int lo = 0, hi = ns - 1;
+              while (lo < hi) {
+                const int mid = (lo + hi) >> 1;
+                if (seg_dg[mid] < d) lo = mid + 1; else hi = mid;
+              }
+              const int pos = seg_off[lo] + atomicAdd(&seg_cur[lo], 1);
+              cand[pos] = key;
+              cand_v[pos] = ((uint32_t)cell << 24) | (uint32_t)(a.sp.off[s] + i);
+            } else {
+              atomicAdd(&hist[lower_edges(d) * ncell + cell], 1);
+            }
+          }
+          c += dr;
+          r += dq;
+          if (c >= cols) { c -= cols; ++r; }
+        }
+      }
+      __syncthreads();
+      direct_rank(f_shift);
+      // ---- the kept tokens: equal keys at an edge split by visual index
+      if (tid < n_c) {
+        const uint32_t key = cand[tid];
+        const uint32_t v = cand_v[tid] & 0xFFFFFFu;
+        const int cell = (int)(cand_v[tid] >> 24);
+        const uint32_t d = (key >> f_shift) & (uint32_t)(f_nb - 1);
+        int sg = 0;
+        while (sg + 1 < ns && seg_off[sg + 1] <= tid) ++sg;
+        const int j0 = seg_off[sg], j_end = j0 + seg_cnt[sg];
+        int bin = lower_edges(d);
+        for (int b = 0; b < n_t; ++b) {
+          const uint32_t tkb = t_key[b];
+          if (((tkb >> f_shift) & (uint32_t)(f_nb - 1)) != d) continue;
+          if (key > tkb) {
+            ++bin;
+          } else if (key == tkb) {
+            if (t_eq[b] == 1) {
+              ++bin;       // the edge's own token, the only one with its key
+            } else {
+              int pos = 0;   // equal keys before this token in visual order
+              for (int j = j0; j < j_end; ++j) pos += cand[j] == key && (cand_v[j] & 0xFFFFFFu) < v;
+              bin += pos >= t_rank[b];
+            }
+          }
+        }
+        atomicAdd(&hist[bin * ncell + cell], 1);
+      }
+      __syncthreads();
+    } else {
     // ---- joint histogram of (bin, cell), spans in order, row-major inside
     // a span (the visual-token order the ranking's tie rule refers to)
-    const int ncell = M * M;
     for (int i = tid; i < K * ncell; i += kThreads) hist[i] = 0;
     bool any_tie = false;
     for (int b = 0; b < n_t; ++b) any_tie |= (t_eq[b] > 1);
@@ -504,6 +604,7 @@ __device__ void stats_body(const StatsArgs& a) {
       }
     }
     __syncthreads();
+    }
     // ---- plug-in MI from the counts (fixed summation order)
     if (tid < K) {
       int sum = 0;
