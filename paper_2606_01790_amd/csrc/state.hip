@@ -334,7 +334,17 @@ __device__ void stats_body(const StatsArgs& a) {
         while (u < nu && u_hi[u] != h) ++u;
         if (u < nu) atomicAdd(&hist[u * nb + ((key >> shift) & (nb - 1))], 1);
       };
-      if (compact) {
+      if (first && cached) {
+        // every key shares the prefix: one histogram, eight keys in flight
+        for (int i0 = tid; i0 < N; i0 += 8 * kThreads) {
+          uint32_t kv[8];
+#pragma unroll
+          for (int u = 0; u < 8; ++u) kv[u] = kc[min(i0 + u * kThreads, N - 1)];
+#pragma unroll
+          for (int u = 0; u < 8; ++u)
+            if (i0 + u * kThreads < N) atomicAdd(&hist[(kv[u] >> shift) & (nb - 1)], 1);
+        }
+      } else if (compact) {
         for (int i = tid; i < n_c; i += kThreads) count(cand[i]);
       } else if (cached) {
         for (int i = tid; i < N; i += kThreads) count(kc[i]);

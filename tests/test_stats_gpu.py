@@ -170,3 +170,25 @@ def test_all_scores_equal_and_two_levels():
     S[0, 1] = np.where(rng.random(Lp) < 0.3, 1e-3, 4e-3).astype(np.float32)
     sbar = np.full(Lp, 1e-3, np.float32)
     run_stats("equal keys", [S, S], sbar, spans, 4, sk.params_default())
+
+
+def test_ties_at_edges_with_few_candidates():
+    """Continuous scores (few keys share the edges' first-digit buckets) with
+    exact three-way ties at every edge rank, scattered over the frames: the
+    equal keys at an edge split by visual index."""
+    rng = np.random.default_rng(12)
+    spans, Lp = layout(3, 20, 30)
+    is_vis = O.visual_metadata(spans, Lp)[0]
+    vis = np.nonzero(is_vis)[0]
+    N, K = vis.size, 8
+    S = np.empty((1, 2, Lp), np.float32)
+    for g in range(2):
+        vals = np.sort(rng.uniform(1e-3, 2e-2, N).astype(np.float32))
+        for b in range(1, K):
+            r = -(-b * N // K)
+            vals[r - 1:r + 2] = vals[r]        # three equal keys around the edge
+        row = rng.uniform(1e-3, 2e-2, Lp).astype(np.float32)
+        row[vis[rng.permutation(N)]] = vals
+        S[0, g] = row
+    sbar = rng.uniform(1e-4, 1e-2, Lp).astype(np.float32)
+    run_stats("edge ties", [S, S], sbar, spans, 3, sk.params_default())
