@@ -74,6 +74,15 @@ __device__ inline float rescale(float m, float mn, float ms, float scale) {
   return m == mn ? 1.0f : __builtin_amdgcn_exp2f(fmaf(m, scale, -ms));
 }
 
+// The value lane l ^ 32 holds.  v_permlane32_swap exchanges the upper lane
+// half of its first operand with the lower half of its second, so with both
+// operands = v the first result holds the lower half's values in the upper
+// lanes and the second the upper half's values in the lower lanes.
+__device__ inline float other_half(float v, int half) {
+  const auto sw = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+  return __uint_as_float(half ? sw[0] : sw[1]);
+}
+
 // Work item of a scoring block: (chunk, group, layer).  Blocks are dealt to
 // the 8 XCDs round-robin by id, so the id is permuted to give every XCD a
 // contiguous range of items: the chunks of one (layer, group) then share
@@ -224,7 +233,7 @@ __global__ __launch_bounds__(NRB * 64) void score_pass1(ScoreArgs a) {
     buf ^= 1;
   }
   // the two lane halves hold the same query row over other tokens
-  const float mo = __shfl_xor(m, 32), lo = __shfl_xor(l, 32);
+  const float mo = other_half(m, half), lo = other_half(l, half);
   const float mn = fmaxf(m, mo);
   const float ms = mn * a.scale;
   l = l * rescale(m, mn, ms, a.scale) + lo * rescale(mo, mn, ms, a.scale);
@@ -259,8 +268,8 @@ __device__ inline float merge_row(const ScoreArgs& a, const float2* part, int r)
 // ---------------------------------------------------------------- pass 2
 // Query rows on the MFMA M axis: each lane owns one token of the 32-token
 // block and sums 2^(y - c_r) over the 16 rows of the wave's row block it
-// holds (c_r in registers); lane halves and then waves are added in a fixed
-// order through LDS.  Each block first merges its group's chunk statistics
+// holds (c_r in registers); the two lane halves are added by a lane swap,
+// then the waves in a fixed order through LDS.  Each block first merges its group's chunk statistics
 // into c_r (one row per thread) while its first K tile is in flight.
 template <typename T, int D, int NRB>
 __global__ __launch_bounds__(NRB * 64) void score_pass2(ScoreArgs a) {
@@ -315,8 +324,11 @@ __global__ __launch_bounds__(NRB * 64) void score_pass2(ScoreArgs a) {
       float tsum = 0.f;
 #pragma unroll
       for (int e = 0; e < 16; ++e) tsum += __builtin_amdgcn_exp2f(fmaf(acc[e], a.scale, -c[e]));
-      tsum += __shfl_xor(tsum, 32);
-      if (half == 0) rs[wave * KS::kRows + 32 * b + l32] = tsum;
+      // add the other lane half's rows through a VALU lane swap (a shuffle
+      // would round-trip through LDS and wait on the fragment reads); both
+      // halves then hold the same sum and store it to the same address
+      tsum += other_half(tsum, half);
+      rs[wave * KS::kRows + 32 * b + l32] = tsum;
     }
     if (more) { STARKV_STAGE_STORE(KS, NRB * 64, sr, kbuf + (buf ^ 1) * KS::kElems) }
     __syncthreads();
