@@ -40,9 +40,9 @@
 extern "C" {
 #endif
 
-#define STARKV_ABI_VERSION 1
+#define STARKV_ABI_VERSION 2
 #define STARKV_MAX_SPANS 64   /* visual spans per call */
-#define STARKV_MAX_GROUPS 64  /* KV groups G */
+#define STARKV_MAX_GROUPS 64  /* KV groups G, and scoring subspaces */
 
 typedef enum starkv_status {
   STARKV_OK = 0,
@@ -68,7 +68,18 @@ typedef enum starkv_dtype {
  * n_layers >= 1; G >= 1, G <= STARKV_MAX_GROUPS, H % G == 0; d in {64, 128};
  * 1 <= W < L; L <= 2^26; the window rows of one group, R = W*H/G, must
  * satisfy R <= 512 and R*(d*elem_bytes + 16) <= 128 KiB (R rounded up to 32);
- * for STARKV_F32, R <= 128. */
+ * for STARKV_F32, R <= 128.
+ *
+ * Subspaces (sec. 3.1; granularity ablation in sec. 4.2): the unit that
+ * gets its own score row, MI prior, stability mean and g* candidate.
+ *   per_head = 0: one subspace per KV group, Ns = G (the GQA default);
+ *   per_head = 1: one subspace per query head, Ns = H, the heads of a group
+ *                 all reading that group's shared K (the paper's MHA-head
+ *                 granularity on a GQA model: K/V replicated across the heads
+ *                 of the group, here without copying them).  Requires
+ *                 H <= STARKV_MAX_GROUPS and W % 8 == 0.
+ * Under MHA (G == H) both settings give the same subspaces.  Every buffer
+ * documented below as per subspace has Ns rows. */
 typedef struct starkv_dims {
   int32_t n_layers;
   int32_t H;
@@ -77,6 +88,7 @@ typedef struct starkv_dims {
   int32_t L;
   int32_t W;
   int32_t dtype;    /* starkv_dtype of q, k and v */
+  int32_t per_head; /* 0: Ns = G subspaces (default), 1: Ns = H */
 } starkv_dims;
 
 /* Element strides of a K or V cache.  Element (layer, group, token, j) is
@@ -125,7 +137,7 @@ typedef struct starkv_span {
 
 /* Per-layer scalar block written by starkv_update_state and read by
  * starkv_select: float32 array [n_layers][starkv_scalars_count(dims)].
- * Within one layer, for G groups:
+ * Within one layer, for the Ns subspaces (written G here):
  *   [0, G)     MI_g of this step                  (Eq. MI)
  *   [G, 2G)    MI_bar_g after the EMA update
  *   [2G, 3G)   prior weights w_g                  (sec. 3.4)
@@ -160,8 +172,8 @@ size_t starkv_scalars_count(const starkv_dims* dims);
 
 /* Bytes of the per-layer online state for all n_layers (sec. 3.2: O(L)
  * per-layer statistics kept across the steps of one trajectory).  The state
- * holds MI_bar[G], the stability means m_g (one entry per token of the
- * current frame, up to frame_cap) and the step count.  It is a plain device
+ * holds MI_bar and the stability mean m_g of every subspace (m_g: one entry
+ * per token of the current frame, up to frame_cap) and the step count.  It is a plain device
  * block the caller may copy out and back to checkpoint a trajectory. */
 size_t starkv_state_bytes(const starkv_dims* dims, int32_t frame_cap);
 
@@ -175,15 +187,16 @@ starkv_status starkv_state_init(const starkv_dims* dims, void* state,
 /* ------------------------------------------------------------------ */
 
 /* Window attention scoring (sec. 3.3, Eq. A_raw and Eq. base_score;
- * Algorithm 1, base-score lines).  For each layer and group g:
+ * Algorithm 1, base-score lines).  For each layer and subspace g:
  *   A_raw[h,t] = sum_{i<W} softmax_t(Q[h,i] . K[g(h),t] / sqrt(d)), t < L_p,
  *   A = AvgPool1D(A_raw) (odd width, zero padding, divide by the width),
- *   S[g,t] = mean of A[h,t] over the heads of g,
+ *   S[g,t] = mean of A[h,t] over the heads of subspace g (the heads of KV
+ *            group g, or head g alone when dims->per_head),
  *   sbar[t] = mean_g S[g,t],  gstar[t] = argmax_g S[g,t] (lowest g on ties).
  * q:     device, [n_layers][H][W][d] contiguous, dims->dtype.  Row i is the
  *        query of token L - W + i.
- * k:     device cache with layout *k_layout, dims->dtype.
- * S:     device out, float32 [n_layers][G][L_p].
+ * k:     device cache with layout *k_layout, dims->dtype (G KV groups).
+ * S:     device out, float32 [n_layers][Ns][L_p].
  * sbar:  device out, float32 [n_layers][L_p].
  * gstar: device out, uint8 [n_layers][L_p].
  * ws:    device workspace of ws_bytes >= starkv_workspace_bytes(dims).
@@ -215,6 +228,7 @@ starkv_status starkv_score(const starkv_dims* dims, const starkv_params* params,
  * state:   device, from starkv_state_init with the same dims and frame_cap;
  *          the current frame's rows*cols must be <= frame_cap (E_STATE).
  * scalars: device out, float32 [n_layers][starkv_scalars_count(dims)].
+ * Every per-group quantity above is per subspace (Ns of them).
  * Errors: E_NULL, E_SHAPE, E_SPANS, E_PARAM, E_STATE, E_WORKSPACE, E_HIP. */
 starkv_status starkv_update_state(const starkv_dims* dims,
                                   const starkv_params* params,
@@ -226,7 +240,7 @@ starkv_status starkv_update_state(const starkv_dims* dims,
 
 /* Final score and global top-B (Eq. final_score in sec. 3.2, sec. 3.5
  * discount, sec. 3.7 selection; Algorithm 1, fusion and selection lines):
- *   beta_t = (1 - lambda_eff) + lambda_eff * G * w[gstar_t],
+ *   beta_t = (1 - lambda_eff) + lambda_eff * Ns * w[gstar_t],
  *   D_t    = d_min + (1 - d_min) exp(-delta (F - f(t)) phi[gstar_t]) on visual
  *            tokens, 1 elsewhere,
  *   s_t    = max(sbar_t beta_t D_t, 0)^(1/T) (no power when 1/T == 1),
@@ -243,7 +257,8 @@ starkv_status starkv_select(const starkv_dims* dims, const starkv_params* params
                             int32_t frame, int32_t B, float* s, int32_t* idx,
                             void* ws, size_t ws_bytes, void* stream);
 
-/* Gather-compaction (sec. 3.7; Algorithm 1, return line):
+/* Gather-compaction (sec. 3.7; Algorithm 1, return line), over the G KV
+ * groups whatever the subspaces:
  *   K'[g] = [K[g, idx[0..B)]; K[g, L_p..L)],  V' likewise.
  * k, v:   device caches with layout *kv_layout (both use it), dims->dtype.
  * idx:    device, int32 [n_layers][B], every entry in [0, L_p); ascending

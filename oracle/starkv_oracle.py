@@ -130,6 +130,18 @@ def group_scores(A: np.ndarray, G: int) -> np.ndarray:
     return S
 
 
+def per_head_cache(K: np.ndarray, H: int) -> np.ndarray:
+    """The MHA-head granularity on a GQA model (sec. 4.2, subspace granularity
+    ablation): each shared key (or value) group is replicated across the H/G
+    query heads that read it, so the cache has H groups with g(h) = h and
+    every head is its own subspace (sec. 3.1: G = H recovers MHA).
+
+    K: [G, L, d] -> [H, L, d], group g's rows repeated for heads
+    [g H/G, (g+1) H/G)."""
+    G = K.shape[0]
+    return np.repeat(np.asarray(K), H // G, axis=0)
+
+
 def base_score(S: np.ndarray):
     """sbar_t = (1/G) sum_g S[g, t] (Eq. base_score) and the token binding
     g*(t) = argmax_g S[g, t] (sec. 3.4).  Reading: argmax ties go to the

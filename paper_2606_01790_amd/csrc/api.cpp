@@ -68,13 +68,13 @@ size_t starkv_workspace_bytes(const starkv_dims* dims) {
 size_t starkv_scalars_count(const starkv_dims* dims) {
   Geometry g;
   if (check_dims(dims, &g) != STARKV_OK) return 0;
-  return scalars_count(g.G);
+  return scalars_count(g.Ns);
 }
 
 size_t starkv_state_bytes(const starkv_dims* dims, int32_t frame_cap) {
   Geometry g;
   if (check_dims(dims, &g) != STARKV_OK || frame_cap < 0) return 0;
-  return state_stride(g.G, frame_cap) * (size_t)g.n_layers;
+  return state_stride(g.Ns, frame_cap) * (size_t)g.n_layers;
 }
 
 starkv_status starkv_state_init(const starkv_dims* dims, void* state,

@@ -23,11 +23,13 @@ struct Geometry {
   int Rpad;     // R rounded up to the 32-row MFMA block
   int esz;      // element bytes
   int dtype;
+  int Ns;       // scoring subspaces: G, or H when per_head
+  int hps;      // query heads per subspace, H / Ns
 };
 
 struct WsLayout {
   size_t part_off;   // float2 [n_layers][G][n_chunks_max][Rpad]  row stats
-  size_t sraw_off;   // float  [n_layers][G][Lp]                  S before pooling
+  size_t sraw_off;   // float  [n_layers][Ns][Lp]                 S before pooling
   size_t total;
 };
 

@@ -9,9 +9,10 @@ namespace starkv {
 namespace {
 
 // ---------------------------------------------------------------- pooling
-// S[g,t] = (1/(k*H/G)) sum_{|j|<=k/2} S_raw[g,t+j] (zero outside [0,L_p)),
-// sbar = mean over groups, g* = first argmax.  The pooled sum adds the k
-// window values in token order.
+// S[g,t] = (1/(k*hps)) sum_{|j|<=k/2} S_raw[g,t+j] (zero outside [0,L_p))
+// for each of the G scoring subspaces (hps heads each), sbar = mean over
+// subspaces, g* = first argmax.  The pooled sum adds the k window values in
+// token order.
 __global__ __launch_bounds__(256) void score_aggregate(const float* sraw, float* S,
                                                        float* sbar, uint8_t* gstar,
                                                        int G, int Lp, int radius,
@@ -76,6 +77,18 @@ int launch_score(const Geometry& g, const starkv_params& p, const void* q,
   a.chunk = chunk;
   a.n_chunks = (g.Lp + chunk - 1) / chunk;
   a.scale = kLog2e / sqrtf((float)g.d);
+  // per-head subspaces: head h of group g owns rows [h*W, (h+1)*W) of the
+  // group's window rows, i.e. W/32 whole row blocks, or W/8 of the 8-row
+  // groups a wave keeps apart
+  a.Ns = g.Ns;
+  a.n_out = g.Ns / g.G;
+  if (a.n_out == 1) {
+    a.n_part = 1;
+    a.upo = g.Rpad / 32;
+  } else {
+    a.n_part = g.W % 32 == 0 ? 1 : 4;
+    a.upo = g.W / (32 / a.n_part);
+  }
   a.part = reinterpret_cast<float2*>(static_cast<char*>(ws) + wl.part_off);
   a.sraw = reinterpret_cast<float*>(static_cast<char*>(ws) + wl.sraw_off);
 
@@ -83,17 +96,17 @@ int launch_score(const Geometry& g, const starkv_params& p, const void* q,
                                          : run_score_f32(a, g.d, g.n_layers, st);
   if (err) return err;
   const int radius = p.pool_kernel / 2;
-  const float inv_norm = 1.0f / ((float)p.pool_kernel * (float)(g.H / g.G));
+  const float inv_norm = 1.0f / ((float)p.pool_kernel * (float)g.hps);
   dim3 ag((g.Lp + 255) / 256, g.n_layers);
-  const size_t lds = (size_t)g.G * (256 + 2 * radius) * sizeof(float);
+  const size_t lds = (size_t)g.Ns * (256 + 2 * radius) * sizeof(float);
   static bool configured = false;   // one-time, idempotent
   if (!configured) {
     hipFuncSetAttribute(reinterpret_cast<const void*>(&score_aggregate),
                         hipFuncAttributeMaxDynamicSharedMemorySize, 160 * 1024);
     configured = true;
   }
-  score_aggregate<<<ag, 256, lds, st>>>(a.sraw, S, sbar, gstar, g.G, g.Lp, radius,
-                                        inv_norm, 1.0f / (float)g.G);
+  score_aggregate<<<ag, 256, lds, st>>>(a.sraw, S, sbar, gstar, g.Ns, g.Lp, radius,
+                                        inv_norm, 1.0f / (float)g.Ns);
   return (int)hipGetLastError();
 }
 

@@ -30,7 +30,11 @@ struct ScoreArgs {
   int chunk, n_chunks, n_chunks_max;
   float scale;          // log2(e) / sqrt(d)
   float2* part;         // [n_layers][G][n_chunks_max][Rpad]  (M, l)
-  float* sraw;          // [n_layers][G][Lp]
+  float* sraw;          // [n_layers][Ns][Lp]
+  // pass-2 output per KV group: n_out subspaces (1, or H/G per head), each
+  // the sum of upo stored partials; a wave stores n_part partials per token
+  // (1: its 32 rows, 4: one per 8-row group)
+  int n_out, upo, n_part, Ns;
 };
 
 namespace {
@@ -268,10 +272,15 @@ __device__ inline float merge_row(const ScoreArgs& a, const float2* part, int r)
 // ---------------------------------------------------------------- pass 2
 // Query rows on the MFMA M axis: each lane owns one token of the 32-token
 // block and sums 2^(y - c_r) over the 16 rows of the wave's row block it
-// holds (c_r in registers); the two lane halves are added by a lane swap,
-// then the waves in a fixed order through LDS.  Each block first merges its group's chunk statistics
-// into c_r (one row per thread) while its first K tile is in flight.
-template <typename T, int D, int NRB>
+// holds (c_r in registers), or four partial sums of its 8-row groups when
+// heads are narrower than the row block; the two lane halves are added by a
+// lane swap, then the partials of each output subspace in a fixed order
+// through LDS.  Each block first merges its
+// group's chunk statistics into c_r (one row per thread) while its first K
+// tile is in flight.
+// SUB: several subspaces per KV group (per-head scores); otherwise the
+// block writes one sum per token and the layout fields are not read.
+template <typename T, int D, int NRB, bool SUB>
 __global__ __launch_bounds__(NRB * 64) void score_pass2(ScoreArgs a) {
   using M = Mfma<T>;
   using KS = KStage<T, D, NRB * 64>;
@@ -287,7 +296,9 @@ __global__ __launch_bounds__(NRB * 64) void score_pass2(ScoreArgs a) {
   const T* kg = group_k<T>(a, layer, g);
   const int t_begin = chunk * a.chunk;
   const int t_end = min(t_begin + a.chunk, a.Lp);
-  float* srow = a.sraw + (size_t)(layer * a.G + g) * a.Lp;
+  const int n_part = SUB ? a.n_part : 1;
+  float* srow = SUB ? a.sraw + ((size_t)layer * a.Ns + (size_t)g * a.n_out) * a.Lp
+                    : a.sraw + (size_t)(layer * a.G + g) * a.Lp;
 
   __shared__ __align__(16) float cs[NRB * 32];
   i32x4 sr[KS::kPerThread];
@@ -314,30 +325,54 @@ __global__ __launch_bounds__(NRB * 64) void score_pass2(ScoreArgs a) {
     const bool more = t0 + KS::kRows < t_end;
     if (more) { STARKV_STAGE_FETCH(KS, NRB * 64, sr, kg, a.ts, t0 + KS::kRows, a.Lp, t0 + 2 * KS::kRows <= a.Lp) }
     const T* tile = kbuf + buf * KS::kElems;
-    float* rs = red + buf * (NRB * KS::kRows);
+    float* rs = red + buf * (NRB * n_part * KS::kRows);
 #pragma unroll
     for (int b = 0; b < KS::kRows / 32; ++b) {
       const T* krow = tile + (32 * b + l32) * KS::kStride;
       f32x16 acc = {};
 #pragma unroll
       for (int kk = 0; kk < NK; ++kk) acc = M::mma(qf[kk], M::load(krow, kk, half), acc);
-      float tsum = 0.f;
+      // the other lane half's rows are added through a VALU lane swap (a
+      // shuffle would round-trip through LDS and wait on the fragment
+      // reads); both halves then hold the same sum and store it to the same
+      // address
+      if (n_part == 1) {
+        float v = 0.f;
 #pragma unroll
-      for (int e = 0; e < 16; ++e) tsum += __builtin_amdgcn_exp2f(fmaf(acc[e], a.scale, -c[e]));
-      // add the other lane half's rows through a VALU lane swap (a shuffle
-      // would round-trip through LDS and wait on the fragment reads); both
-      // halves then hold the same sum and store it to the same address
-      tsum += other_half(tsum, half);
-      rs[wave * KS::kRows + 32 * b + l32] = tsum;
+        for (int e = 0; e < 16; ++e) v += __builtin_amdgcn_exp2f(fmaf(acc[e], a.scale, -c[e]));
+        v += other_half(v, half);
+        rs[wave * KS::kRows + 32 * b + l32] = v;
+      } else {
+        // one partial per 8-row group: rows 8i + 4*half + (0..3) here
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          float v = 0.f;
+#pragma unroll
+          for (int j = 0; j < 4; ++j)
+            v += __builtin_amdgcn_exp2f(fmaf(acc[4 * i + j], a.scale, -c[4 * i + j]));
+          rs[(wave * 4 + i) * KS::kRows + 32 * b + l32] = v + other_half(v, half);
+        }
+      }
     }
     if (more) { STARKV_STAGE_STORE(KS, NRB * 64, sr, kbuf + (buf ^ 1) * KS::kElems) }
     __syncthreads();
-    for (int i = threadIdx.x; i < KS::kRows; i += NRB * 64) {
-      if (t0 + i < t_end) {
-        float sum = 0.f;
+    if (!SUB) {           // one subspace per group: all NRB wave sums
+      for (int i = threadIdx.x; i < KS::kRows; i += NRB * 64) {
+        if (t0 + i < t_end) {
+          float sum = 0.f;
 #pragma unroll
-        for (int w = 0; w < NRB; ++w) sum += rs[w * KS::kRows + i];
-        srow[t0 + i] = sum;
+          for (int w = 0; w < NRB; ++w) sum += rs[w * KS::kRows + i];
+          srow[t0 + i] = sum;
+        }
+      }
+    } else {              // per head: upo consecutive partials per head
+      for (int it = threadIdx.x; it < a.n_out * KS::kRows; it += NRB * 64) {
+        const int o = it / KS::kRows, i = it % KS::kRows;
+        if (t0 + i < t_end) {
+          float sum = 0.f;
+          for (int u = o * a.upo; u < (o + 1) * a.upo; ++u) sum += rs[u * KS::kRows + i];
+          srow[(size_t)o * a.Lp + t0 + i] = sum;
+        }
       }
     }
     buf ^= 1;
@@ -349,9 +384,12 @@ int run_passes(const ScoreArgs& a, int n_layers, hipStream_t st) {
   using KS = KStage<T, D, NRB * 64>;
   const int items = a.n_chunks * a.G * n_layers;
   const size_t lds1 = 2 * (size_t)KS::kElems * sizeof(T);
-  const size_t lds2 = lds1 + 2 * (size_t)NRB * KS::kRows * sizeof(float);
+  const size_t lds2 = lds1 + 2 * (size_t)NRB * a.n_part * KS::kRows * sizeof(float);
   score_pass1<T, D, NRB><<<items, NRB * 64, lds1, st>>>(a);
-  score_pass2<T, D, NRB><<<items, NRB * 64, lds2, st>>>(a);
+  if (a.n_out > 1)
+    score_pass2<T, D, NRB, true><<<items, NRB * 64, lds2, st>>>(a);
+  else
+    score_pass2<T, D, NRB, false><<<items, NRB * 64, lds2, st>>>(a);
   return (int)hipGetLastError();
 }
 

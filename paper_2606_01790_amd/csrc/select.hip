@@ -297,10 +297,10 @@ int launch_select(const Geometry& g, const starkv_params& p, const float* sbar,
   a.scal = scalars;
   a.s = s;
   a.idx = idx;
-  a.G = g.G;
+  a.G = g.Ns;   // g* indexes the scoring subspaces
   a.Lp = g.Lp;
   a.B = B;
-  a.sc = (int)scalars_count(g.G);
+  a.sc = (int)scalars_count(g.Ns);
   a.frame = frame;
   a.cache = g.Lp < kLdsKeys ? g.Lp : kLdsKeys;
   a.delta = p.delta;

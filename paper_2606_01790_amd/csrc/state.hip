@@ -743,15 +743,16 @@ int launch_update_state(const Geometry& g, const starkv_params& p,
   a.sbar = sbar;
   a.scal = scalars;
   a.state = static_cast<char*>(state);
-  a.state_stride = state_stride(g.G, frame_cap);
-  a.m_off = state_m_off(g.G);
-  a.G = g.G;
+  // every per-group statistic here is per scoring subspace
+  a.state_stride = state_stride(g.Ns, frame_cap);
+  a.m_off = state_m_off(g.Ns);
+  a.G = g.Ns;
   a.Lp = g.Lp;
   a.nbins = p.n_bins;
   a.grid = p.grid;
   a.cur = current_span(spans, n_spans, frame);
   a.frame_cap = frame_cap;
-  a.sc = (int)scalars_count(g.G);
+  a.sc = (int)scalars_count(g.Ns);
   a.rho_t = p.rho_t;
   a.eps = p.eps;
   a.sp.n = n_spans;
@@ -773,7 +774,7 @@ int launch_update_state(const Geometry& g, const starkv_params& p,
   f.scal = scalars;
   f.state = a.state;
   f.state_stride = a.state_stride;
-  f.G = g.G;
+  f.G = g.Ns;
   f.sc = a.sc;
   f.nf = a.cur >= 0 ? spans[a.cur].rows * spans[a.cur].cols : -1;
   f.rho_mi = p.rho_mi;
@@ -784,14 +785,14 @@ int launch_update_state(const Geometry& g, const starkv_params& p,
   f.t_max = p.t_max;
   f.n_warmup = p.n_warmup;
   f.n_ramp = p.n_ramp;
-  stats_kernel<<<dim3(g.G + 2, g.n_layers), kThreads, kStatsLds, st>>>(a);
+  stats_kernel<<<dim3(g.Ns + 2, g.n_layers), kThreads, kStatsLds, st>>>(a);
   return (int)hipGetLastError();
 }
 
 int launch_state_init(const Geometry& g, void* state, int32_t frame_cap, void* stream) {
   hipStream_t st = reinterpret_cast<hipStream_t>(stream);
   state_init_kernel<<<g.n_layers, 256, 0, st>>>(static_cast<char*>(state),
-                                                state_stride(g.G, frame_cap), g.G,
+                                                state_stride(g.Ns, frame_cap), g.Ns,
                                                 frame_cap);
   return (int)hipGetLastError();
 }

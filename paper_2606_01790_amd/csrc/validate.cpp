@@ -27,6 +27,10 @@ starkv_status check_dims(const starkv_dims* dims, Geometry* g) {
   const int64_t Rpad = (R + 31) / 32 * 32;
   if (Rpad > 512 || Rpad * (d * esz + 16) > kMaxQBytes) return STARKV_E_SHAPE;
   if (esz == 4 && Rpad > 128) return STARKV_E_SHAPE;   // float32: up to 4 row blocks
+  // per-head subspaces: a head's window rows must be whole 8-row groups of
+  // the MFMA output, and the subspaces must fit the statistics kernels
+  if (dims->per_head != 0 && dims->per_head != 1) return STARKV_E_SHAPE;
+  if (dims->per_head && (H > STARKV_MAX_GROUPS || W % 8 != 0)) return STARKV_E_SHAPE;
   if (g) {
     g->n_layers = (int)nl;
     g->H = (int)H;
@@ -39,6 +43,8 @@ starkv_status check_dims(const starkv_dims* dims, Geometry* g) {
     g->Rpad = (int)Rpad;
     g->esz = (int)esz;
     g->dtype = dims->dtype;
+    g->Ns = dims->per_head ? (int)H : (int)G;
+    g->hps = (int)(H / g->Ns);
   }
   return STARKV_OK;
 }
@@ -121,7 +127,7 @@ WsLayout ws_layout(const Geometry& g) {
   const size_t lg = (size_t)g.n_layers * g.G;
   w.part_off = 0;
   w.sraw_off = up256(lg * max_chunks(g) * g.Rpad * 2 * sizeof(float));
-  w.total = w.sraw_off + up256(lg * g.Lp * sizeof(float));
+  w.total = w.sraw_off + up256((size_t)g.n_layers * g.Ns * g.Lp * sizeof(float));
   return w;
 }
 

@@ -55,11 +55,11 @@ class LayerGroups:
             if prev_scored is not None:
                 st.wait_event(prev_scored)
             dims = make_dims(l1 - l0)
-            G, Lp, W, d = dims.G, dims.L - dims.W, dims.W, dims.d
+            G, Ns, Lp, W, d = dims.G, dims.Ns, dims.L - dims.W, dims.W, dims.d
             kg, vg = K[l0:l1], V[l0:l1]
             lay = sk.contiguous_layout(kg, dims)
             n_out = G * (B + W) * d
-            Sg = S[l0 * G * Lp:l1 * G * Lp]
+            Sg = S[l0 * Ns * Lp:l1 * Ns * Lp]
             sb = sbar[l0 * Lp:l1 * Lp]
             gs = gstar[l0 * Lp:l1 * Lp]
             scg = scal[l0 * nscal:l1 * nscal]
@@ -82,9 +82,11 @@ class TrajectoryRunner:
     """Holds every device buffer of a trajectory of `spec` and runs its steps."""
 
     def __init__(self, spec: WorkloadSpec, params: sk.Params, device="cuda",
-                 max_budget: int | None = None):
+                 max_budget: int | None = None, per_head: bool = False):
         self.spec = spec
         self.params = params
+        self.per_head = per_head
+        self.Ns = spec.H if per_head else spec.G   # scoring subspaces
         self.device = torch.device(device)
         self.traj = Trajectory(spec)
         sp = spec
@@ -101,7 +103,7 @@ class TrajectoryRunner:
         self.V = torch.zeros((nl, G, self.L_cap, d), dtype=self.tdtype, device=dev)
         self.Q = torch.zeros((nl, H, W, d), dtype=self.tdtype, device=dev)
         self.layout = sk.contiguous_layout(self.K, self.dims(sp.steps))
-        self.S = torch.zeros(nl * G * Lp_max, dtype=torch.float32, device=dev)
+        self.S = torch.zeros(nl * self.Ns * Lp_max, dtype=torch.float32, device=dev)
         self.sbar = torch.zeros(nl * Lp_max, dtype=torch.float32, device=dev)
         self.gstar = torch.zeros(nl * Lp_max, dtype=torch.uint8, device=dev)
         self.s = torch.zeros(nl * Lp_max, dtype=torch.float32, device=dev)
@@ -118,7 +120,8 @@ class TrajectoryRunner:
 
     def dims(self, step: int) -> sk.Dims:
         sp = self.spec
-        return sk.make_dims(sp.n_layers, sp.H, sp.G, sp.d, sp.L(step), sp.W, self.dt)
+        return sk.make_dims(sp.n_layers, sp.H, sp.G, sp.d, sp.L(step), sp.W, self.dt,
+                            self.per_head)
 
     def reset(self, stream=None):
         """Start a trajectory: fresh online state."""
@@ -171,9 +174,11 @@ class TrajectoryRunner:
         sp = self.spec
         if getattr(self, "_groups", None) is None or len(self._groups.ranges) != groups:
             self._groups = LayerGroups(sp.n_layers, groups, self.ws.numel(), self.device)
-        d1 = sk.make_dims(1, sp.H, sp.G, sp.d, sp.L(sp.steps), sp.W, self.dt)
+        d1 = sk.make_dims(1, sp.H, sp.G, sp.d, sp.L(sp.steps), sp.W, self.dt,
+                          self.per_head)
         self._groups.run(
-            lambda n: sk.make_dims(n, sp.H, sp.G, sp.d, sp.L(step), sp.W, self.dt),
+            lambda n: sk.make_dims(n, sp.H, sp.G, sp.d, sp.L(step), sp.W, self.dt,
+                                   self.per_head),
             self.params, step, sp.spans(step), B, self.Q, self.K, self.V, self.S,
             self.sbar, self.gstar, self.s, self.idx, self.k_out, self.v_out, self.scal,
             self.nscal, self.state, sk.state_bytes(d1, self.frame_cap), self.frame_cap)
@@ -184,7 +189,7 @@ class TrajectoryRunner:
         nl, G, Lp, W, d = sp.n_layers, sp.G, sp.L_p(step), sp.W, sp.d
         n_out = nl * G * (B + W) * d
         out = dict(
-            S=self.S[:nl * G * Lp].view(nl, G, Lp).cpu().numpy(),
+            S=self.S[:nl * self.Ns * Lp].view(nl, self.Ns, Lp).cpu().numpy(),
             sbar=self.sbar[:nl * Lp].view(nl, Lp).cpu().numpy(),
             gstar=self.gstar[:nl * Lp].view(nl, Lp).cpu().numpy(),
             s=self.s[:nl * Lp].view(nl, Lp).cpu().numpy(),
@@ -211,8 +216,10 @@ class ArrayCase:
     """
 
     def __init__(self, H, G, d, W, n_layers, L_cap, dtype, params, frame_cap,
-                 device="cuda"):
+                 device="cuda", per_head=False):
         self.H, self.G, self.d, self.W, self.nl = H, G, d, W, n_layers
+        self.per_head = per_head
+        self.Ns = H if per_head else G
         self.L_cap, self.dtype, self.params = L_cap, dtype, params
         self.dt = sk.BF16 if dtype == "bf16" else sk.F32
         self.device = torch.device(device)
@@ -226,7 +233,8 @@ class ArrayCase:
         self.reset()
 
     def dims(self, L):
-        return sk.make_dims(self.nl, self.H, self.G, self.d, L, self.W, self.dt)
+        return sk.make_dims(self.nl, self.H, self.G, self.d, L, self.W, self.dt,
+                            self.per_head)
 
     def reset(self):
         sk.state_init(self.dims(self.L_cap), self.state, self.frame_cap)
@@ -239,7 +247,7 @@ class ArrayCase:
         k = to_device(K, self.dtype, dev)
         v = to_device(V, self.dtype, dev)
         lay = sk.contiguous_layout(k, dims)
-        S = torch.zeros(nl * G * Lp, dtype=torch.float32, device=dev)
+        S = torch.zeros(nl * self.Ns * Lp, dtype=torch.float32, device=dev)
         sbar = torch.zeros(nl * Lp, dtype=torch.float32, device=dev)
         gstar = torch.zeros(nl * Lp, dtype=torch.uint8, device=dev)
         s = torch.zeros(nl * Lp, dtype=torch.float32, device=dev)
@@ -254,7 +262,7 @@ class ArrayCase:
         sk.select(dims, self.params, sbar, gstar, self.scal, spans, F, B, s, idx, ws)
         sk.compact(dims, k, v, lay, idx, B, ko, vo)
         torch.cuda.synchronize()
-        out = dict(S=S.view(nl, G, Lp).cpu().numpy(), sbar=sbar.view(nl, Lp).cpu().numpy(),
+        out = dict(S=S.view(nl, self.Ns, Lp).cpu().numpy(), sbar=sbar.view(nl, Lp).cpu().numpy(),
                    gstar=gstar.view(nl, Lp).cpu().numpy(), s=s.view(nl, Lp).cpu().numpy(),
                    idx=idx[:nl * B].view(nl, B).cpu().numpy(),
                    scal=self.scal.view(nl, self.nscal).cpu().numpy())

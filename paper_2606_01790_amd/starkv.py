@@ -31,11 +31,16 @@ STATUS = {
 class Dims(ctypes.Structure):
     _fields_ = [("n_layers", c_int32), ("H", c_int32), ("G", c_int32),
                 ("d", c_int32), ("L", c_int32), ("W", c_int32),
-                ("dtype", c_int32)]
+                ("dtype", c_int32), ("per_head", c_int32)]
 
     @property
     def Lp(self) -> int:
         return self.L - self.W
+
+    @property
+    def Ns(self) -> int:
+        """Scoring subspaces: one per KV group, or one per head."""
+        return self.H if self.per_head else self.G
 
 
 class KVLayout(ctypes.Structure):
@@ -114,8 +119,8 @@ def _check(fn: str, code: int):
 
 # ------------------------------------------------------------------ helpers
 
-def make_dims(n_layers, H, G, d, L, W, dtype) -> Dims:
-    return Dims(n_layers, H, G, d, L, W, dtype)
+def make_dims(n_layers, H, G, d, L, W, dtype, per_head=False) -> Dims:
+    return Dims(n_layers, H, G, d, L, W, dtype, 1 if per_head else 0)
 
 
 def params_default() -> Params:
@@ -200,7 +205,7 @@ def score(dims: Dims, params: Params, q, k, k_layout: KVLayout, S, sbar, gstar,
     nl, Lp = dims.n_layers, dims.Lp
     _need(q, nl * dims.H * dims.W * dims.d * _esz(dims), "q")
     _need_cache(k, dims, k_layout, "k")
-    _need(S, nl * dims.G * Lp * 4, "S")
+    _need(S, nl * dims.Ns * Lp * 4, "S")
     _need(sbar, nl * Lp * 4, "sbar")
     _need(gstar, nl * Lp, "gstar")
     _need(ws, workspace_bytes(dims), "ws")
@@ -213,7 +218,7 @@ def score(dims: Dims, params: Params, q, k, k_layout: KVLayout, S, sbar, gstar,
 def update_state(dims: Dims, params: Params, S, sbar, spans, frame: int, state,
                  frame_cap: int, scalars, ws=None, stream=None):
     arr, n = spans_array(spans)
-    _need(S, dims.n_layers * dims.G * dims.Lp * 4, "S")
+    _need(S, dims.n_layers * dims.Ns * dims.Lp * 4, "S")
     _need(sbar, dims.n_layers * dims.Lp * 4, "sbar")
     _need(scalars, dims.n_layers * scalars_count(dims) * 4, "scalars")
     _need(state, state_bytes(dims, frame_cap), "state")

@@ -40,7 +40,7 @@ def test_header_symbols_are_exported():
 
 def test_abi_version_and_status_strings():
     L = sk.lib()
-    assert L.starkv_abi_version() == 1
+    assert L.starkv_abi_version() == 2
     assert L.starkv_status_str(0) == b"ok"
     assert b"budget" in L.starkv_status_str(3)
 
@@ -80,6 +80,24 @@ def test_sizes():
     assert sk.workspace_bytes(dims(G=3)) == 0          # H % G != 0
 
 
+def test_sizes_per_head():
+    """Per-head subspaces (Ns = H): S, the scalar block and the state have a
+    row per head; the pass-1 row statistics stay per KV group."""
+    d = dims(per_head=True)
+    assert d.Ns == 28
+    assert sk.scalars_count(d) == 4 * 28 + 4
+    per = (64 + 28 * 4 + 28 * 2691 * 4 + 255) // 256 * 256
+    assert sk.state_bytes(d, 2691) == 28 * per
+    Lp = 13711 - 32
+    chunks = (Lp + 255) // 256
+    up = lambda x: (x + 255) // 256 * 256  # noqa: E731
+    assert sk.workspace_bytes(d) == up(28 * 4 * chunks * 224 * 8) + up(28 * 28 * Lp * 4)
+    # MHA: both settings describe the same subspaces
+    m0, m1 = dims(G=28, W=8), dims(G=28, W=8, per_head=True)
+    assert (sk.workspace_bytes(m0), sk.scalars_count(m0)) == \
+        (sk.workspace_bytes(m1), sk.scalars_count(m1))
+
+
 @pytest.mark.parametrize("kw,code", [
     (dict(G=3), "E_SHAPE"),
     (dict(d=96), "E_SHAPE"),
@@ -88,6 +106,8 @@ def test_sizes():
     (dict(n_layers=0), "E_SHAPE"),
     (dict(dtype=7), "E_DTYPE"),
     (dict(W=80), "E_SHAPE"),       # 80*7 = 560 window rows > 512
+    (dict(W=12, per_head=True), "E_SHAPE"),    # a head's rows not whole 8-row groups
+    (dict(H=72, G=4, W=8, per_head=True), "E_SHAPE"),   # 72 subspaces > 64
 ])
 def test_score_rejects_bad_dims(kw, code):
     d = dims(**kw)
@@ -96,6 +116,13 @@ def test_score_rejects_bad_dims(kw, code):
     rc = sk.lib().starkv_score(ctypes.byref(d), ctypes.byref(p), FAKE, FAKE,
                                ctypes.byref(lay), FAKE, FAKE, FAKE, FAKE, 1 << 40, None)
     assert sk.STATUS[rc] == code
+
+
+def test_score_rejects_unknown_subspace_mode():
+    d = dims()
+    d.per_head = 2
+    assert _score(d) == "E_SHAPE"
+    assert sk.workspace_bytes(d) == 0
 
 
 def _score(d, p=None, lay=None, q=FAKE, k=FAKE, ws=FAKE, ws_bytes=1 << 40):

@@ -127,6 +127,38 @@ def test_group_scores_are_head_means():
     np.testing.assert_allclose(S, [[1.5] * 5, [3.5] * 5], rtol=1e-15)
 
 
+def test_per_head_cache_gives_each_head_its_own_attention():
+    """MHA-head granularity on a GQA model (sec. 4.2 ablation): with K
+    replicated per head, the per-head window mass equals the GQA model's own
+    per-head mass (every head still reads its group's keys), and S = A."""
+    r = rng(21)
+    H, G, W, L, d = 6, 2, 3, 11, 8
+    Q = r.standard_normal((H, W, d))
+    K = r.standard_normal((G, L, d))
+    Kh = O.per_head_cache(K, H)
+    assert Kh.shape == (H, L, d)
+    for h in range(H):
+        np.testing.assert_array_equal(Kh[h], K[h * G // H])
+    A_gqa = O.window_attention_mass(Q, K)        # heads read group h G / H
+    A_mha = O.window_attention_mass(Q, Kh)       # head h reads its own copy
+    np.testing.assert_allclose(A_mha, A_gqa, rtol=1e-14)
+    S = O.group_scores(A_mha, H)
+    np.testing.assert_allclose(S, A_gqa, rtol=1e-14)
+
+
+def test_group_scores_are_means_of_per_head_scores():
+    """The GQA-group score of a group is the mean of its heads' per-head
+    scores (Eq. base_score is linear in A), pooled or not."""
+    r = rng(22)
+    H, G, W, L, d = 8, 2, 4, 40, 16
+    Q = r.standard_normal((H, W, d))
+    K = r.standard_normal((G, L, d))
+    A = O.avg_pool1d(O.window_attention_mass(Q, K), 5)
+    S_group = O.group_scores(A, G)
+    S_head = O.group_scores(O.avg_pool1d(O.window_attention_mass(Q, O.per_head_cache(K, H)), 5), H)
+    np.testing.assert_allclose(S_head.reshape(G, H // G, L).mean(axis=1), S_group, rtol=1e-13)
+
+
 def test_base_score_single_group_and_ties():
     S = rng(8).random((1, 6))
     sbar, gstar = O.base_score(S)

@@ -51,16 +51,20 @@ class HostFrames:
         return np.concatenate(ks + [k], axis=1), np.concatenate(vs + [v], axis=1)
 
 
-def run_trajectory(cid, layers=None, prior_active=False, steps=None, groups=1):
+def run_trajectory(cid, layers=None, prior_active=False, steps=None, groups=1,
+                   per_head=False):
+    """per_head: a subspace per query head; the oracle then scores the cache
+    with every shared K group replicated across its heads."""
     spec = WL.SPECS[cid]
     p = params_for(cid, prior_active)
     op = oracle_params(p)
-    say(f"cfg{cid} prior_active={prior_active}: allocate")
-    runner = TrajectoryRunner(spec, p)
+    say(f"cfg{cid} prior_active={prior_active} per_head={per_head}: allocate")
+    runner = TrajectoryRunner(spec, p, per_head=per_head)
     runner.reset()
     host = HostFrames(spec)
     layers = list(range(spec.n_layers)) if layers is None else list(layers)
-    states = {l: O.LayerState(spec.G) for l in layers}
+    Ns = spec.H if per_head else spec.G
+    states = {l: O.LayerState(Ns) for l in layers}
     report = {}
     for step in range(1, (steps or spec.steps) + 1):
         say(f"cfg{cid} step {step}: load + score/update")
@@ -77,8 +81,11 @@ def run_trajectory(cid, layers=None, prior_active=False, steps=None, groups=1):
         for layer in layers:
             K, V = host.cache(layer, step)
             Q = host.tr.window_q(layer, step)
+            Ks = WL.to_float64(K, spec.dtype)
+            if per_head:
+                Ks = O.per_head_cache(Ks, spec.H)
             out, states[layer] = O.compress_layer(
-                WL.to_float64(Q, spec.dtype), WL.to_float64(K, spec.dtype), None, L, W,
+                WL.to_float64(Q, spec.dtype), Ks, None, L, W,
                 spans, step, budgets[0], op, states[layer], copy_rows=(K, V))
             orc_base[layer] = (out, K, V)
         for B in budgets:
@@ -94,7 +101,7 @@ def run_trajectory(cid, layers=None, prior_active=False, steps=None, groups=1):
                 orc["K_out"], orc["V_out"] = O.gather_compact(K, V, orc["I"], L, W)
                 g = {k: v[layer] for k, v in gpu.items()}
                 check_layer(f"cfg{cid} step{step} L{layer} B{B}", K, V, L, W, spans,
-                            step, B, op, spec.G, g, orc, report)
+                            step, B, op, Ns, g, orc, report)
     say(f"cfg{cid} done: max S rel {max(report['S']):.2e}, max s rel "
         f"{max(report['s']):.2e}, idx band tokens {sum(report['idx_band'])}, "
         f"g* near-ties {sum(report['gstar_ties'])}")
@@ -243,25 +250,31 @@ def test_graph_replay_matches_eager():
 # ------------------------------------------------------------------ edge cases
 
 def run_case(tag, H, G, d, W, L, spans, F, B, dtype, p, seed=0, n_layers=2,
-             L_cap=None, Qs=None, Ks=None, Vs=None, case=None, states=None):
+             L_cap=None, Qs=None, Ks=None, Vs=None, case=None, states=None,
+             per_head=False):
     L_cap = L_cap or L
     if Qs is None:
         Qs, Ks, Vs = WL.random_case(seed, n_layers, H, G, d, L_cap, W, dtype)
     frame_cap = max([r * c for (_, r, c, _) in spans] + [1])
-    case = case or ArrayCase(H, G, d, W, n_layers, L_cap, dtype, p, frame_cap)
-    say(f"{tag}: H={H} G={G} d={d} W={W} L={L} B={B} {dtype}")
+    case = case or ArrayCase(H, G, d, W, n_layers, L_cap, dtype, p, frame_cap,
+                             per_head=per_head)
+    say(f"{tag}: H={H} G={G} d={d} W={W} L={L} B={B} {dtype} per_head={per_head}")
     gpu = case.run(Qs, Ks, Vs, L, spans, F, B)
     op = oracle_params(p)
-    states = states if states is not None else [O.LayerState(G) for _ in range(n_layers)]
+    Ns = H if per_head else G
+    states = states if states is not None else [O.LayerState(Ns) for _ in range(n_layers)]
     report = {}
     for layer in range(n_layers):
         K = Ks[layer][:, :L]
         V = Vs[layer][:, :L]
+        Kq = WL.to_float64(K, dtype)
+        if per_head:
+            Kq = O.per_head_cache(Kq, H)
         out, states[layer] = O.compress_layer(
-            WL.to_float64(Qs[layer], dtype), WL.to_float64(K, dtype), None, L, W, spans,
+            WL.to_float64(Qs[layer], dtype), Kq, None, L, W, spans,
             F, B, op, states[layer], copy_rows=(K, V))
         g = {k: v[layer] for k, v in gpu.items()}
-        check_layer(f"{tag} L{layer}", K, V, L, W, spans, F, B, op, G, g, out, report)
+        check_layer(f"{tag} L{layer}", K, V, L, W, spans, F, B, op, Ns, g, out, report)
     return case, states
 
 
@@ -329,3 +342,48 @@ def test_frame_size_change_resets_stability():
                                 "bf16", p, n_layers=2, Qs=Qs, Ks=Ks, Vs=Vs, case=case,
                                 states=states)
     assert states[0].m.shape == (2, 180)
+
+
+# ------------------------------------------------- per-head subspaces (MHA-head)
+
+def test_per_head_config2_shape():
+    """Qwen2.5-VL-7B shape (H=28 over G=4 groups, W=32, one 1920x1080 frame):
+    28 subspaces, one per head, every pass-2 row block a whole head."""
+    spec = WL.SPECS[2]
+    p = params_for(2, prior_active=True)
+    spans = spec.spans(1)
+    run_case("per-head cfg2", spec.H, spec.G, spec.d, spec.W, spec.L(1), spans, 1,
+             spec.budgets(1)[0], "bf16", p, seed=31, n_layers=1, per_head=True)
+
+
+@pytest.mark.parametrize("H,G,W,dtype,d", [(4, 2, 8, "f32", 64), (28, 4, 16, "bf16", 128),
+                                           (14, 2, 40, "bf16", 64), (8, 2, 64, "bf16", 128)])
+def test_per_head_window_row_layouts(H, G, W, dtype, d):
+    """Heads of W = 8, 16 and 40 rows (partials per 8-row group, a head split
+    across row blocks at W = 40) and of W = 64 (two whole row blocks)."""
+    p = params_for(2, prior_active=True)
+    spans = [(5, 12, 15, 1), (200, 12, 15, 2)]
+    L = 420 + W
+    run_case(f"per-head W={W}", H, G, d, W, L, spans, 2, 97, dtype, p, seed=W,
+             per_head=True)
+
+
+def test_per_head_trajectory_state():
+    """Five steps of the 28-layer trajectory with per-head subspaces: the MI
+    EMA and the stability means of 28 subspaces carried across steps."""
+    run_trajectory(3, layers=[0, 27], prior_active=True, per_head=True)
+
+
+def test_per_head_flag_is_identity_under_mha():
+    """G = H: a subspace per group and per head are the same thing, so both
+    settings give bit-identical outputs."""
+    p = params_for(2, prior_active=True)
+    spans = [(0, 10, 12, 1)]
+    outs = []
+    for ph in (False, True):
+        Qs, Ks, Vs = WL.random_case(41, 2, 4, 4, 64, 300, 8, "bf16")
+        case = ArrayCase(4, 4, 64, 8, 2, 300, "bf16", p, 120, per_head=ph)
+        say(f"mha per_head={ph}")
+        outs.append(case.run(Qs, Ks, Vs, 300, spans, 1, 50))
+    for k in outs[0]:
+        assert np.array_equal(outs[0][k], outs[1][k]), k
