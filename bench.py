@@ -52,6 +52,9 @@ def parse():
                          "writes 1 GiB (the calibration of the HBM byte counters)")
     ap.add_argument("--no-per-call", action="store_true",
                     help="skip the per-call timing (no roofline; for counter runs)")
+    ap.add_argument("--per-head", action="store_true",
+                    help="a scoring subspace per query head (the MHA-head granularity "
+                         "on the GQA model) instead of one per KV group")
     return ap.parse_args()
 
 
@@ -62,14 +65,16 @@ def log(msg):
 class Workload:
     """Resident inputs and outputs of one trajectory of `spec`."""
 
-    def __init__(self, spec, params, n_states, device="cuda"):
+    def __init__(self, spec, params, n_states, device="cuda", per_head=False):
         import torch
         from paper_2606_01790_amd import starkv as sk
         from paper_2606_01790_amd.pipeline import to_device
         from paper_2606_01790_amd.workload import Trajectory
 
         self.spec, self.params, self.sk = spec, params, sk
+        self.per_head = per_head
         sp = spec
+        Ns = sp.H if per_head else sp.G
         dt = torch.bfloat16 if sp.dtype == "bf16" else torch.float32
         self.dt = sk.BF16 if sp.dtype == "bf16" else sk.F32
         tr = Trajectory(sp)
@@ -100,7 +105,7 @@ class Workload:
         del frames_k, frames_v
         Lp, B = sp.L_p(sp.steps), max(max(sp.budgets(s)) for s in range(1, sp.steps + 1))
         f32 = torch.float32
-        self.S = torch.empty(nl * G * Lp, dtype=f32, device=device)
+        self.S = torch.empty(nl * Ns * Lp, dtype=f32, device=device)
         self.sbar = torch.empty(nl * Lp, dtype=f32, device=device)
         self.gstar = torch.empty(nl * Lp, dtype=torch.uint8, device=device)
         self.s = torch.empty(nl * Lp, dtype=f32, device=device)
@@ -118,9 +123,10 @@ class Workload:
             sk.state_init(dmax, st, nf)
         torch.cuda.synchronize()
 
-    def dims(self, s):
+    def dims(self, s, n_layers=None):
         sp = self.spec
-        return self.sk.make_dims(sp.n_layers, sp.H, sp.G, sp.d, sp.L(s), sp.W, self.dt)
+        return self.sk.make_dims(n_layers or sp.n_layers, sp.H, sp.G, sp.d, sp.L(s), sp.W,
+                                 self.dt, self.per_head)
 
     def trajectory(self, state, groups=1):
         """The hot path over the whole trajectory: the four calls per step, for
@@ -130,12 +136,11 @@ class Workload:
             from paper_2606_01790_amd.pipeline import LayerGroups
             if getattr(self, "_lg", None) is None or len(self._lg.ranges) != groups:
                 self._lg = LayerGroups(sp.n_layers, groups, self.ws.numel(), self.ws.device)
-            d1 = sk.make_dims(1, sp.H, sp.G, sp.d, sp.L(sp.steps), sp.W, self.dt)
-            stride = sk.state_bytes(d1, self.frame_cap)
+            stride = sk.state_bytes(self.dims(sp.steps, 1), self.frame_cap)
             for s in range(1, sp.steps + 1):
                 i = s - 1
                 self._lg.run(
-                    lambda n, s=s: sk.make_dims(n, sp.H, sp.G, sp.d, sp.L(s), sp.W, self.dt),
+                    lambda n, s=s: self.dims(s, n),
                     p, s, sp.spans(s), sp.budgets(s)[0], self.Q[i], self.K[i], self.V[i],
                     self.S, self.sbar, self.gstar, self.s, self.idx, self.k_out, self.v_out,
                     self.scal, self.nscal, state, stride, self.frame_cap)
@@ -155,16 +160,17 @@ class Workload:
                        self.v_out)
 
 
-def call_bytes(spec, s, name):
+def call_bytes(spec, s, name, per_head=False):
     """Algorithmic HBM bytes of one call at trajectory step s, all layers:
-    inputs read once and outputs written once."""
+    inputs read once and outputs written once (Ns scoring subspaces)."""
     sp = spec
     e, nl, H, G, d, W = sp.elem_bytes, sp.n_layers, sp.H, sp.G, sp.d, sp.W
+    Ns = H if per_head else G
     Lp, nv, nf, B = sp.L_p(s), sp.n_vis(s), sp.n_frame, sp.budgets(s)[0]
     if name == "score":        # Q, K_past in; S, sbar, g* out
-        per = e * (H * W * d + G * Lp * d) + 4 * G * Lp + 4 * Lp + Lp
+        per = e * (H * W * d + G * Lp * d) + 4 * Ns * Lp + 4 * Lp + Lp
     elif name == "update_state":   # S of visual tokens, sbar, stability means
-        per = 4 * G * nv + 4 * Lp + 4 * G * nf * 3
+        per = 4 * Ns * nv + 4 * Lp + 4 * Ns * nf * 3
     elif name == "select":     # sbar, g* in; s, idx out
         per = 5 * Lp + 4 * Lp + 4 * B
     else:                      # idx in; B+W rows of K and V in and out
@@ -209,7 +215,7 @@ def per_call_timing(wl, spec, sk, torch, reps):
             d = per.setdefault(name, {"time": 0.0, "launches": 0, "bytes": 0})
             d["time"] += e0.elapsed_time(e1) * 1e-3
             d["launches"] += reps
-            d["bytes"] += reps * call_bytes(spec, s, name)
+            d["bytes"] += reps * call_bytes(spec, s, name, wl.per_head)
     return per
 
 
@@ -232,7 +238,8 @@ def main():
         params.t_min, params.t_max = 0.95, 1.05
     log(f"workload {spec.name}: building resident inputs")
     n_states = args.warmup + 3
-    wl = Workload(spec, params, n_states)
+    wl = Workload(spec, params, n_states, per_head=args.per_head)
+    workload = spec.name + ("-per-head" if args.per_head else "")
     layer_tokens = spec.n_layers * sum(spec.n_vis(s) for s in range(1, spec.steps + 1))
     bytes_alg = spec.n_layers * sum(WL.bytes_alg(spec, s, spec.budgets(s)[0])
                                     for s in range(1, spec.steps + 1))
@@ -289,7 +296,7 @@ def main():
         achieved = avg_b / avg_s / 1e9
         roofline = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS,
                     "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
-                    "traffic": measured_traffic(f"starkv_{dom}", spec.name),
+                    "traffic": measured_traffic(f"starkv_{dom}", workload),
                     "kernel": f"starkv_{dom}",
                     "avg_launch_us": round(avg_s * 1e6, 2),
                     "alg_bytes_per_launch": int(avg_b)}
@@ -297,7 +304,7 @@ def main():
 
     cpu = None
     if not args.no_cpu_baseline:
-        cpu = cpu_baseline(spec, params, args.cpu_seconds)
+        cpu = cpu_baseline(spec, params, args.cpu_seconds, args.per_head)
 
     line = {
         "metric": METRIC,
@@ -312,8 +319,10 @@ def main():
         "vs_baseline": None,
         "dtype": spec.dtype,
         "data": "synthetic",
-        "config": {"workload": spec.name, "n_layers": spec.n_layers, "H": spec.H,
+        "config": {"workload": workload, "n_layers": spec.n_layers, "H": spec.H,
                    "G": spec.G, "d": spec.d, "W": spec.W,
+                   "subspaces": (f"per head ({spec.H})" if args.per_head
+                                 else f"per KV group ({spec.G})"),
                    "trajectory_steps": spec.steps, "budget_pct": list(spec.pcts),
                    "layer_tokens_per_step": layer_tokens,
                    "bytes_alg_per_step": bytes_alg,
@@ -371,7 +380,7 @@ def measured_traffic(call, workload):
         return None
 
 
-def cpu_baseline(spec, params, seconds):
+def cpu_baseline(spec, params, seconds, per_head=False):
     """The fp64 oracle, untuned, on the host cores: whole trajectories (every
     step, fresh state) of layers 0, 1, 2, ... of the same workload, cycling
     through the layers again if needed, until `seconds` of oracle time have
@@ -401,9 +410,11 @@ def cpu_baseline(spec, params, seconds):
             K, V = tr.layer_cache(layer, s)
             steps.append((s, WL.to_float64(tr.window_q(layer, s), spec.dtype),
                           WL.to_float64(K, spec.dtype), K, V))
-        state = O.LayerState(spec.G)
+        state = O.LayerState(spec.H if per_head else spec.G)
         t0 = time.perf_counter()
         for s, Q, K64, K, V in steps:
+            if per_head:
+                K64 = O.per_head_cache(K64, spec.H)
             _, state = O.compress_layer(Q, K64, None, spec.L(s), spec.W, spec.spans(s), s,
                                         spec.budgets(s)[0], op, state, copy_rows=(K, V))
             tokens += spec.n_vis(s)
@@ -413,7 +424,8 @@ def cpu_baseline(spec, params, seconds):
     return {"value": round(tokens / spent, 1), "unit": "layer-tokens/s", "cores": threads,
             "kind": "oracle",
             "sample": f"{runs} whole {spec.steps}-step layer trajectories of {spec.name} "
-                      f"(layers 0-{min(runs, spec.n_layers) - 1}; {tokens} layer-tokens, "
+                      + ("with per-head subspaces " if per_head else "")
+                      + f"(layers 0-{min(runs, spec.n_layers) - 1}; {tokens} layer-tokens, "
                       f"{spent:.1f} s of oracle time; numpy fp64, BLAS threads {threads})"}
 
 
