@@ -79,13 +79,14 @@ class Workload:
         self.dt = sk.BF16 if sp.dtype == "bf16" else sk.F32
         tr = Trajectory(sp)
         nl, G, H, d, W, nf = sp.n_layers, sp.G, sp.H, sp.d, sp.W, sp.n_frame
-        frames_k = torch.empty((sp.steps, nl, G, nf, d), dtype=dt, device=device)
-        frames_v = torch.empty_like(frames_k)
+        frames_k, frames_v = {}, {}     # frame -> [n_layers, G, tokens, d]
         for f in range(1, sp.steps + 1):
+            frames_k[f] = torch.empty((nl, G, sp.frame_tokens(f), d), dtype=dt, device=device)
+            frames_v[f] = torch.empty_like(frames_k[f])
             for layer in range(nl):
                 k, v = tr.frame_kv(layer, f)
-                frames_k[f - 1, layer] = to_device(k, sp.dtype, device)
-                frames_v[f - 1, layer] = to_device(v, sp.dtype, device)
+                frames_k[f][layer] = to_device(k, sp.dtype, device)
+                frames_v[f][layer] = to_device(v, sp.dtype, device)
         self.K, self.V, self.Q, self.layout = [], [], [], []
         for s in range(1, sp.steps + 1):
             tk = torch.empty((nl, G, sp.text, d), dtype=dt, device=device)
@@ -96,14 +97,14 @@ class Workload:
                 tk[layer] = to_device(k, sp.dtype, device)
                 tv[layer] = to_device(v, sp.dtype, device)
                 q[layer] = to_device(tr.window_q(layer, s), sp.dtype, device)
-            K = torch.cat([frames_k[f] for f in range(s)] + [tk], dim=2).contiguous()
-            V = torch.cat([frames_v[f] for f in range(s)] + [tv], dim=2).contiguous()
+            K = torch.cat([frames_k[f] for f in sp.frames(s)] + [tk], dim=2).contiguous()
+            V = torch.cat([frames_v[f] for f in sp.frames(s)] + [tv], dim=2).contiguous()
             self.K.append(K)
             self.V.append(V)
             self.Q.append(q)
             self.layout.append(sk.contiguous_layout(K, self.dims(s)))
         del frames_k, frames_v
-        Lp, B = sp.L_p(sp.steps), max(max(sp.budgets(s)) for s in range(1, sp.steps + 1))
+        Lp, B = sp.L_p(sp.peak_step), max(max(sp.budgets(s)) for s in range(1, sp.steps + 1))
         f32 = torch.float32
         self.S = torch.empty(nl * Ns * Lp, dtype=f32, device=device)
         self.sbar = torch.empty(nl * Lp, dtype=f32, device=device)
@@ -112,7 +113,7 @@ class Workload:
         self.idx = torch.empty(nl * B, dtype=torch.int32, device=device)
         self.k_out = torch.empty(nl * G * (B + W) * d, dtype=dt, device=device)
         self.v_out = torch.empty_like(self.k_out)
-        dmax = self.dims(sp.steps)
+        dmax = self.dims(sp.peak_step)
         self.ws = torch.empty(sk.workspace_bytes(dmax), dtype=torch.uint8, device=device)
         self.nscal = sk.scalars_count(dmax)
         self.scal = torch.empty(nl * self.nscal, dtype=f32, device=device)
@@ -136,7 +137,7 @@ class Workload:
             from paper_2606_01790_amd.pipeline import LayerGroups
             if getattr(self, "_lg", None) is None or len(self._lg.ranges) != groups:
                 self._lg = LayerGroups(sp.n_layers, groups, self.ws.numel(), self.ws.device)
-            stride = sk.state_bytes(self.dims(sp.steps, 1), self.frame_cap)
+            stride = sk.state_bytes(self.dims(sp.peak_step, 1), self.frame_cap)
             for s in range(1, sp.steps + 1):
                 i = s - 1
                 self._lg.run(
@@ -259,7 +260,7 @@ def main():
         # into a HIP graph: the timed region replays it, so the host's Python
         # launch cost does not starve the GPU.
         graph_state = wl.states[-1]
-        dmax = wl.dims(spec.steps)
+        dmax = wl.dims(spec.peak_step)
         g = torch.cuda.CUDAGraph()
         with torch.cuda.graph(g):
             sk.state_init(dmax, graph_state, wl.frame_cap)

@@ -92,8 +92,8 @@ class TrajectoryRunner:
         sp = spec
         self.tdtype = torch.bfloat16 if sp.dtype == "bf16" else torch.float32
         self.dt = sk.BF16 if sp.dtype == "bf16" else sk.F32
-        self.L_cap = sp.L(sp.steps)
-        Lp_max = sp.L_p(sp.steps)
+        self.L_cap = sp.L(sp.peak_step)
+        Lp_max = sp.L_p(sp.peak_step)
         B_max = max_budget if max_budget is not None else max(
             max(sp.budgets(s)) for s in range(1, sp.steps + 1))
         self.B_max = B_max
@@ -102,7 +102,7 @@ class TrajectoryRunner:
         self.K = torch.zeros((nl, G, self.L_cap, d), dtype=self.tdtype, device=dev)
         self.V = torch.zeros((nl, G, self.L_cap, d), dtype=self.tdtype, device=dev)
         self.Q = torch.zeros((nl, H, W, d), dtype=self.tdtype, device=dev)
-        self.layout = sk.contiguous_layout(self.K, self.dims(sp.steps))
+        self.layout = sk.contiguous_layout(self.K, self.dims(sp.peak_step))
         self.S = torch.zeros(nl * self.Ns * Lp_max, dtype=torch.float32, device=dev)
         self.sbar = torch.zeros(nl * Lp_max, dtype=torch.float32, device=dev)
         self.gstar = torch.zeros(nl * Lp_max, dtype=torch.uint8, device=dev)
@@ -110,7 +110,7 @@ class TrajectoryRunner:
         self.idx = torch.zeros(nl * max(B_max, 1), dtype=torch.int32, device=dev)
         self.k_out = torch.zeros(nl * G * (B_max + W) * d, dtype=self.tdtype, device=dev)
         self.v_out = torch.zeros_like(self.k_out)
-        dmax = self.dims(sp.steps)
+        dmax = self.dims(sp.peak_step)
         self.ws = torch.zeros(sk.workspace_bytes(dmax), dtype=torch.uint8, device=dev)
         self.frame_cap = sp.n_frame
         self.state = torch.zeros(sk.state_bytes(dmax, self.frame_cap), dtype=torch.uint8,
@@ -125,12 +125,21 @@ class TrajectoryRunner:
 
     def reset(self, stream=None):
         """Start a trajectory: fresh online state."""
-        sk.state_init(self.dims(self.spec.steps), self.state, self.frame_cap, stream)
+        sk.state_init(self.dims(self.spec.peak_step), self.state, self.frame_cap, stream)
 
     def load_step(self, step: int):
         """Append screenshot `step` and write the step's text tokens and window
         queries for every layer (host -> device copies, outside timing)."""
         sp, tr = self.spec, self.traj
+        if not sp.appends:
+            # frames leave the context or change size: the whole cache moves
+            L = sp.L(step)
+            for layer in range(sp.n_layers):
+                k, v = tr.layer_cache(layer, step)
+                self.K[layer, :, :L] = to_device(k, sp.dtype, self.device)
+                self.V[layer, :, :L] = to_device(v, sp.dtype, self.device)
+                self.Q[layer] = to_device(tr.window_q(layer, step), sp.dtype, self.device)
+            return
         nf = sp.n_frame
         f0 = (step - 1) * nf
         for layer in range(sp.n_layers):
@@ -174,7 +183,7 @@ class TrajectoryRunner:
         sp = self.spec
         if getattr(self, "_groups", None) is None or len(self._groups.ranges) != groups:
             self._groups = LayerGroups(sp.n_layers, groups, self.ws.numel(), self.device)
-        d1 = sk.make_dims(1, sp.H, sp.G, sp.d, sp.L(sp.steps), sp.W, self.dt,
+        d1 = sk.make_dims(1, sp.H, sp.G, sp.d, sp.L(sp.peak_step), sp.W, self.dt,
                           self.per_head)
         self._groups.run(
             lambda n: sk.make_dims(n, sp.H, sp.G, sp.d, sp.L(step), sp.W, self.dt,

@@ -9,9 +9,11 @@ attention, sec. 3.1; single-screenshot grounding and multi-step trajectories
 with one screenshot appended per step, Appendix dataset settings).  None of
 the paper's benchmark data is used or reproduced.
 
-Token layout at trajectory step s (1-based): frames 1..s (each a rows x cols
-raster of visual tokens, row-major), then the step's text tokens; the last W
-text tokens are the observation window.  K, V and Q are standard normal;
+Token layout at trajectory step s (1-based): the frames in the context (1..s,
+or with `slots` image slots only the newest `slots` of them; each a
+rows x cols raster of visual tokens, row-major, at the frame's own
+resolution), then the step's text tokens; the last W text tokens are the
+observation window.  K, V and Q are standard normal;
 each K group carries Gaussian "bumps" over screen regions along a random
 sign vector u, and window queries lean toward their group's u, so attention
 concentrates spatially and the spatial MI is non-zero.
@@ -46,24 +48,59 @@ class WorkloadSpec:
     q_align: float             # window-query lean toward the group's u
     q_scale_range: tuple = None  # per-step Q scale, U[lo, hi], all layers
     seed: int = 0
+    slots: int = 0             # image slots: frames kept in context (0: all)
+    res_change: tuple = ()     # (first_frame, cols, rows): resolution from then on
+
+    def grid(self, f: int):
+        """(cols, rows) of frame f."""
+        cols, rows = self.cols, self.rows
+        for f0, c, r in self.res_change:
+            if f >= f0:
+                cols, rows = c, r
+        return cols, rows
+
+    def frame_tokens(self, f: int) -> int:
+        c, r = self.grid(f)
+        return c * r
 
     @property
     def n_frame(self) -> int:
-        return self.rows * self.cols
+        """The largest frame's token count (capacity of per-frame state)."""
+        return max([self.rows * self.cols] + [c * r for _, c, r in self.res_change])
+
+    def frames(self, s: int):
+        """Frames in the context at step s, oldest first."""
+        first = max(1, s - self.slots + 1) if self.slots else 1
+        return list(range(first, s + 1))
 
     def L(self, s: int) -> int:
-        return s * self.n_frame + self.text
+        return self.n_vis(s) + self.text
 
     def L_p(self, s: int) -> int:
         return self.L(s) - self.W
 
     def n_vis(self, s: int) -> int:
-        return s * self.n_frame
+        return sum(self.frame_tokens(f) for f in self.frames(s))
 
     def spans(self, s: int):
-        """Visual spans (start, rows, cols, frame) at step s; frames 1..s."""
-        return [((f - 1) * self.n_frame, self.rows, self.cols, f)
-                for f in range(1, s + 1)]
+        """Visual spans (start, rows, cols, frame) at step s, in context order."""
+        out, t = [], 0
+        for f in self.frames(s):
+            c, r = self.grid(f)
+            out.append((t, r, c, f))
+            t += r * c
+        return out
+
+    @property
+    def appends(self) -> bool:
+        """Each step's cache is the previous one plus a frame of the same size
+        (old tokens keep their positions)."""
+        return self.slots == 0 and not self.res_change
+
+    @property
+    def peak_step(self) -> int:
+        """The step with the longest cache (buffer sizes are taken there)."""
+        return max(range(1, self.steps + 1), key=lambda s: (self.L(s), -s))
 
     def budgets(self, s: int):
         """B = floor(pct * N_vis / 100) for each budget percentage."""
@@ -90,6 +127,12 @@ SPECS = {
     5: WorkloadSpec("qwen25vl7b-28L-30step-2560x1440", 28, 28, 4, 128, "bf16",
                     91, 51, 30, 1024, 64, (10,), 0.5, 6.0, 3, False, 0.7,
                     0.35, seed=1005),
+    # image_slots = 5 (the multi-step setting of the paper's trajectory
+    # benchmark): from step 6 on the oldest screenshot leaves the context;
+    # from frame 7 on the screen is 1280x720 (46x26 tokens)
+    6: WorkloadSpec("qwen25vl7b-28L-10step-slots5-1080p-720p", 28, 28, 4, 128,
+                    "bf16", 69, 39, 10, 256, 32, (20,), 0.5, 6.0, 1, True, 0.7,
+                    0.35, seed=1006, slots=5, res_change=((7, 46, 26),)),
 }
 
 
@@ -158,11 +201,15 @@ class Trajectory:
         if key in self._centres:
             return self._centres[key]
         r = self._rng(layer, frame, 3)
-        fresh = np.stack([r.random((sp.G, sp.regions)) * sp.cols,
-                          r.random((sp.G, sp.regions)) * sp.rows], axis=-1)
+        cols, rows = sp.grid(frame)
+        fresh = np.stack([r.random((sp.G, sp.regions)) * cols,
+                          r.random((sp.G, sp.regions)) * rows], axis=-1)
         keep = r.random((sp.G, sp.regions)) < sp.repeat_p
         if frame > 1:
             prev = self.centres(layer, frame - 1)
+            pc, pr = sp.grid(frame - 1)
+            if (pc, pr) != (cols, rows):    # same screen place at the new resolution
+                prev = prev * np.array([cols / pc, rows / pr])
             fresh = np.where(keep[..., None], prev, fresh)
         self._centres[key] = fresh
         return fresh
@@ -170,8 +217,9 @@ class Trajectory:
     def _bump_profile(self, layer: int, frame: int) -> np.ndarray:
         """[G, N_F] bump amplitude per visual token (float32)."""
         sp = self.spec
-        rr, cc = np.divmod(np.arange(sp.n_frame), sp.cols)
-        prof = np.zeros((sp.G, sp.n_frame), dtype=np.float64)
+        cols, rows = sp.grid(frame)
+        rr, cc = np.divmod(np.arange(cols * rows), cols)
+        prof = np.zeros((sp.G, cols * rows), dtype=np.float64)
         cen = self.centres(layer, frame)
         for g in range(sp.G):
             if not self._bumped(layer, g):
@@ -185,10 +233,11 @@ class Trajectory:
     def frame_kv(self, layer: int, frame: int):
         """K, V [G, N_F, d] of one screenshot in one layer."""
         sp = self.spec
+        nf = sp.frame_tokens(frame)
         K = self._rng(layer, frame, 0).standard_normal(
-            (sp.G, sp.n_frame, sp.d), dtype=np.float32)
+            (sp.G, nf, sp.d), dtype=np.float32)
         V = self._rng(layer, frame, 1).standard_normal(
-            (sp.G, sp.n_frame, sp.d), dtype=np.float32)
+            (sp.G, nf, sp.d), dtype=np.float32)
         prof = self._bump_profile(layer, frame)
         u = self._u(layer)
         K = K + prof[:, :, None] * u[:, None, :]
@@ -225,7 +274,7 @@ class Trajectory:
         """The assembled cache K, V [G, L, d] of a layer at a step."""
         sp = self.spec
         ks, vs = [], []
-        for f in range(1, step + 1):
+        for f in sp.frames(step):
             k, v = self.frame_kv(layer, f)
             ks.append(k)
             vs.append(v)

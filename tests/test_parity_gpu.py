@@ -41,7 +41,7 @@ class HostFrames:
 
     def cache(self, layer, step):
         ks, vs = [], []
-        for f in range(1, step + 1):
+        for f in self.spec.frames(step):
             if (layer, f) not in self.frames:
                 self.frames[(layer, f)] = self.tr.frame_kv(layer, f)
             k, v = self.frames[(layer, f)]
@@ -52,7 +52,7 @@ class HostFrames:
 
 
 def run_trajectory(cid, layers=None, prior_active=False, steps=None, groups=1,
-                   per_head=False):
+                   per_head=False, on_step=None):
     """per_head: a subspace per query head; the oracle then scores the cache
     with every shared K group replicated across its heads."""
     spec = WL.SPECS[cid]
@@ -102,6 +102,8 @@ def run_trajectory(cid, layers=None, prior_active=False, steps=None, groups=1,
                 g = {k: v[layer] for k, v in gpu.items()}
                 check_layer(f"cfg{cid} step{step} L{layer} B{B}", K, V, L, W, spans,
                             step, B, op, Ns, g, orc, report)
+        if on_step is not None:
+            on_step(step, runner.outputs(step, budgets[-1]), states)
     say(f"cfg{cid} done: max S rel {max(report['S']):.2e}, max s rel "
         f"{max(report['s']):.2e}, idx band tokens {sum(report['idx_band'])}, "
         f"g* near-ties {sum(report['gstar_ties'])}")
@@ -221,7 +223,7 @@ def test_graph_replay_matches_eager():
         r.load_step(s)     # caches hold step 2's text; step 1 only reads frame 1 + text
     # eager reference: steps 1 and 2 on the same buffers as the graph
     def traj():
-        sk.state_init(r.dims(spec.steps), r.state, r.frame_cap)
+        sk.state_init(r.dims(spec.peak_step), r.state, r.frame_cap)
         r.run_step(2, spec.budgets(2)[0])
     say("graph: eager reference")
     traj()
@@ -387,3 +389,25 @@ def test_per_head_flag_is_identity_under_mha():
         outs.append(case.run(Qs, Ks, Vs, 300, spans, 1, 50))
     for k in outs[0]:
         assert np.array_equal(outs[0][k], outs[1][k]), k
+
+
+# ------------------------------------- image slots and a resolution change
+
+def test_config6_image_slots_and_resolution_change():
+    """Ten steps with image_slots = 5 (frames leave the context from step 6,
+    every token after them moves) and the screen switching from 1920x1080 to
+    1280x720 at frame 7.  The stability means follow the newest frame, so
+    phi is exactly 0 at step 1 and at step 7, where the frame's token count
+    changes, and positive in the steps in between and after (S is never
+    orthogonal to the previous means here)."""
+    spec = WL.SPECS[6]
+    G = spec.G
+
+    def on_step(step, gpu, states):
+        phi = gpu["scal"][:, 3 * G:4 * G]
+        if step in (1, 7):
+            assert np.all(phi == 0.0), f"step {step}: phi {phi[:2]}"
+        else:
+            assert np.all(phi > 0.0), f"step {step}: phi {phi[:2]}"
+
+    run_trajectory(6, layers=[0, 1, 27], prior_active=True, on_step=on_step)

@@ -89,3 +89,43 @@ def test_bump_centres_repeat_across_frames():
     for f in range(2, 40):
         same += np.allclose(t.centres(0, f)[0], t.centres(0, f - 1)[0])
     assert 15 <= same <= 37      # about 70% of frames keep their places
+
+
+def test_image_slots_and_resolution_change_bookkeeping():
+    """image_slots = 5 with a 1920x1080 -> 1280x720 switch at frame 7: the
+    context holds the newest five frames, spans tile the visual prefix in
+    frame order, and L, N_vis and B follow the frames actually present."""
+    sp = WL.SPECS[6]
+    assert sp.frames(3) == [1, 2, 3]
+    assert sp.frames(6) == [2, 3, 4, 5, 6]
+    assert sp.frames(10) == [6, 7, 8, 9, 10]
+    assert sp.grid(6) == (69, 39) and sp.grid(7) == (46, 26)
+    assert sp.n_frame == 2691 and not sp.appends
+    for s in range(1, sp.steps + 1):
+        spans = sp.spans(s)
+        t = 0
+        for (start, rows, cols, f), want in zip(spans, sp.frames(s)):
+            assert start == t and f == want and (cols, rows) == sp.grid(f)
+            t += rows * cols
+        assert t == sp.n_vis(s) and sp.L(s) == t + sp.text
+        assert sp.budgets(s) == [20 * t // 100]
+    assert sp.L(10) == 2691 + 4 * 46 * 26 + 256
+    assert sp.peak_step == 5        # steps 5 and 6 tie; the first is taken
+
+
+def test_frames_keep_their_bytes_when_they_move():
+    """A frame's K/V bytes depend only on (layer, frame): after the oldest
+    frames leave the context, frame 7 sits at position 0 .. with its own
+    bytes, and the single-resolution configurations are unchanged by the
+    per-frame grid (frame 3 of config 3 starts at 2 * 2691)."""
+    t6 = WL.Trajectory(WL.SPECS[6])
+    k10, v10 = t6.layer_cache(2, 10)
+    k7, v7 = t6.frame_kv(2, 7)
+    n6 = 2691
+    np.testing.assert_array_equal(k10[:, n6:n6 + 46 * 26], k7)
+    np.testing.assert_array_equal(v10[:, n6:n6 + 46 * 26], v7)
+    k6, _ = t6.frame_kv(2, 6)
+    np.testing.assert_array_equal(k10[:, :n6], k6)
+    t3 = WL.Trajectory(WL.SPECS[3])
+    k, _ = t3.layer_cache(1, 4)
+    np.testing.assert_array_equal(k[:, 2 * 2691:3 * 2691], t3.frame_kv(1, 3)[0])
