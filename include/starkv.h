@@ -271,6 +271,37 @@ starkv_status starkv_compact(const starkv_dims* dims, const void* k,
                              const int32_t* idx, int32_t B, void* k_out,
                              void* v_out, void* stream);
 
+/* ------------------------------------------------------------------ */
+/* after the stage: decode attention over the compressed cache          */
+/* ------------------------------------------------------------------ */
+
+/* Bytes of device workspace starkv_decode needs for these dims and token
+ * count.  0 if they are invalid for it. */
+size_t starkv_decode_workspace_bytes(const starkv_dims* dims, int32_t n_tokens);
+
+/* Decode attention of one new token per query head over a cache of n_tokens
+ * tokens per (layer, KV group), the step whose cost the compression lowers
+ * (sec. 4.3, decode-time efficiency; sec. 3.1 for the GQA map):
+ *   o[h] = sum_{t < n_tokens} softmax_t(q[h] . K[g(h),t] / sqrt(d)) V[g(h),t].
+ * Run on K'/V' from starkv_compact (n_tokens = B + W, layout layer_stride =
+ * G*(B+W)*d, group_stride = (B+W)*d, token_stride = d) it is decoding with
+ * the compressed cache; run on the full cache (n_tokens = L) it is the
+ * uncompressed baseline.  Only n_layers, H, G, d and dtype of dims are read:
+ * STARKV_BF16 only (E_DTYPE otherwise), H/G <= 16, d in {64, 128},
+ * 1 <= n_tokens <= 2^26.
+ * q:      device, bf16 [n_layers][H][d] contiguous.
+ * k, v:   device bf16 caches with layout *kv_layout (both use it).
+ * out:    device out, float32 [n_layers][H][d].
+ * ws:     device workspace of ws_bytes >= starkv_decode_workspace_bytes().
+ * Softmax and accumulation are fp32; the result does not depend on the
+ * launch split beyond the fixed order of its partial sums, and is bitwise
+ * deterministic.  Errors: E_NULL, E_SHAPE, E_DTYPE, E_ALIGN, E_WORKSPACE,
+ * E_HIP. */
+starkv_status starkv_decode(const starkv_dims* dims, const void* q, const void* k,
+                            const void* v, const starkv_kv_layout* kv_layout,
+                            int32_t n_tokens, float* out, void* ws, size_t ws_bytes,
+                            void* stream);
+
 #ifdef __cplusplus
 }
 #endif

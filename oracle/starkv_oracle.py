@@ -417,3 +417,30 @@ def compress_layer(Q, K, V, L: int, W: int, spans, F: int, B: int,
                m=m_new, D=D, h_hat=h_hat, T=T, s_f=s_f, s=s, I=I,
                K_out=K_out, V_out=V_out)
     return out, new_state
+
+
+# --------------------------------------------------------------------------
+# after the stage: decode attention over the (compressed) cache
+# --------------------------------------------------------------------------
+
+def decode_attention(q: np.ndarray, K: np.ndarray, V: np.ndarray) -> np.ndarray:
+    """One decoding step of attention, the cost the compression lowers
+    (sec. 4.3, decode-time efficiency): each query head h attends to every
+    cached token of its group g(h) = floor(h G / H) (sec. 3.1),
+      o[h] = softmax_t(q[h] . K[g(h), t] / sqrt(d)) V[g(h), t].
+
+    q: [H, d]; K, V: [G, n, d] (the compacted K', V' or a full cache).
+    Returns o: [H, d] in fp64."""
+    q = np.asarray(q, dtype=np.float64)
+    K = np.asarray(K, dtype=np.float64)
+    V = np.asarray(V, dtype=np.float64)
+    H, d = q.shape
+    G = K.shape[0]
+    o = np.zeros((H, d), dtype=np.float64)
+    for h in range(H):
+        g = (h * G) // H
+        x = K[g] @ q[h] / math.sqrt(d)
+        p = np.exp(x - x.max())
+        p /= p.sum()
+        o[h] = p @ V[g]
+    return o

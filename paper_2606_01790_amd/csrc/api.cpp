@@ -169,4 +169,32 @@ starkv_status starkv_compact(const starkv_dims* dims, const void* k,
   return hip_status(launch_compact(g, k, v, *kv_layout, idx, B, k_out, v_out, stream));
 }
 
+size_t starkv_decode_workspace_bytes(const starkv_dims* dims, int32_t n_tokens) {
+  DecodeGeometry g;
+  if (check_decode(dims, n_tokens, &g) != STARKV_OK) return 0;
+  return decode_ws_bytes(g);
+}
+
+starkv_status starkv_decode(const starkv_dims* dims, const void* q, const void* k,
+                            const void* v, const starkv_kv_layout* kv_layout,
+                            int32_t n_tokens, float* out, void* ws, size_t ws_bytes,
+                            void* stream) {
+  DecodeGeometry g;
+  starkv_status st = check_decode(dims, n_tokens, &g);
+  if (st != STARKV_OK) return st;
+  if (!q || !k || !v || !kv_layout || !out) return STARKV_E_NULL;
+  const int64_t esz = 2;
+  if (kv_layout->layer_stride < 0 || kv_layout->group_stride < 0 ||
+      kv_layout->token_stride < g.d)
+    return STARKV_E_SHAPE;
+  if ((kv_layout->layer_stride * esz) % 16 || (kv_layout->group_stride * esz) % 16 ||
+      (kv_layout->token_stride * esz) % 16)
+    return STARKV_E_ALIGN;
+  if (!aligned(q, 16) || !aligned(k, 16) || !aligned(v, 16) || !aligned(out, 4))
+    return STARKV_E_ALIGN;
+  if (!ws || ws_bytes < decode_ws_bytes(g)) return STARKV_E_WORKSPACE;
+  if (!aligned(ws, 16)) return STARKV_E_ALIGN;
+  return hip_status(launch_decode(g, q, k, v, *kv_layout, out, ws, stream));
+}
+
 }  // extern "C"

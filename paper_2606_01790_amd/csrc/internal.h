@@ -85,4 +85,15 @@ int launch_compact(const Geometry& g, const void* k, const void* v,
 int launch_state_init(const Geometry& g, void* state, int32_t frame_cap,
                       void* stream);
 
+// Decode attention over a cache of n_tok tokens per (layer, group).
+struct DecodeGeometry {
+  int n_layers, H, G, d, n_tok;
+  int chunk;     // tokens per split block
+  int n_split;   // token splits per (layer, group)
+};
+starkv_status check_decode(const starkv_dims* dims, int32_t n_tokens, DecodeGeometry* g);
+size_t decode_ws_bytes(const DecodeGeometry& g);
+int launch_decode(const DecodeGeometry& g, const void* q, const void* k, const void* v,
+                  const starkv_kv_layout& lay, float* out, void* ws, void* stream);
+
 }  // namespace starkv

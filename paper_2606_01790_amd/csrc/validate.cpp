@@ -1,5 +1,6 @@
 // Host-side argument validation and buffer geometry.  No HIP: this unit is
 // also built with the host compiler for the sanitizer tests.
+#include <algorithm>
 #include <cmath>
 #include <cstdint>
 
@@ -132,6 +133,37 @@ WsLayout ws_layout(const Geometry& g) {
 }
 
 size_t scalars_count(int G) { return 4 * (size_t)G + 4; }
+
+starkv_status check_decode(const starkv_dims* dims, int32_t n_tokens, DecodeGeometry* g) {
+  if (!dims) return STARKV_E_NULL;
+  if (dims->dtype != STARKV_F32 && dims->dtype != STARKV_BF16) return STARKV_E_DTYPE;
+  if (dims->dtype != STARKV_BF16) return STARKV_E_DTYPE;   // bf16 caches only
+  const int64_t H = dims->H, G = dims->G, d = dims->d, nl = dims->n_layers;
+  if (nl < 1 || nl > 4096) return STARKV_E_SHAPE;
+  if (G < 1 || G > STARKV_MAX_GROUPS || H < G || H % G != 0 || H / G > 16)
+    return STARKV_E_SHAPE;
+  if (d != 64 && d != 128) return STARKV_E_SHAPE;
+  if (n_tokens < 1 || n_tokens > kMaxL) return STARKV_E_SHAPE;
+  if (g) {
+    g->n_layers = (int)nl;
+    g->H = (int)H;
+    g->G = (int)G;
+    g->d = (int)d;
+    g->n_tok = n_tokens;
+    // about 1024 tokens per block, at most ~2048 blocks in all
+    const int64_t cap = std::max<int64_t>(1, 2048 / (nl * G));
+    int64_t ns = std::min<int64_t>((n_tokens + 1023) / 1024, cap);
+    int64_t chunk = (n_tokens + ns - 1) / ns;
+    chunk = (chunk + 31) / 32 * 32;
+    g->chunk = (int)chunk;
+    g->n_split = (int)((n_tokens + chunk - 1) / chunk);
+  }
+  return STARKV_OK;
+}
+
+size_t decode_ws_bytes(const DecodeGeometry& g) {
+  return up256((size_t)g.n_layers * g.G * g.n_split * (g.H / g.G) * (g.d + 2) * sizeof(float));
+}
 
 size_t state_mibar_off() { return sizeof(StateHeader); }
 size_t state_m_off(int G) {

@@ -92,6 +92,10 @@ SIGNATURES = {
     "starkv_compact": (c_int32, [POINTER(Dims), c_void_p, c_void_p,
                                  POINTER(KVLayout), c_void_p, c_int32, c_void_p,
                                  c_void_p, c_void_p]),
+    "starkv_decode_workspace_bytes": (c_size_t, [POINTER(Dims), c_int32]),
+    "starkv_decode": (c_int32, [POINTER(Dims), c_void_p, c_void_p, c_void_p,
+                                POINTER(KVLayout), c_int32, c_void_p, c_void_p, c_size_t,
+                                c_void_p]),
 }
 
 
@@ -255,3 +259,22 @@ def compact(dims: Dims, k, v, kv_layout: KVLayout, idx, B: int, k_out, v_out,
     _check("starkv_compact", lib().starkv_compact(
         ctypes.byref(dims), _ptr(k), _ptr(v), ctypes.byref(kv_layout), _ptr(idx),
         B, _ptr(k_out), _ptr(v_out), _stream(stream)))
+
+
+def decode_workspace_bytes(dims: Dims, n_tokens: int) -> int:
+    return int(lib().starkv_decode_workspace_bytes(ctypes.byref(dims), n_tokens))
+
+
+def decode(dims: Dims, q, k, v, kv_layout: KVLayout, n_tokens: int, out, ws, stream=None):
+    """Decode attention of one token per head over n_tokens cached tokens."""
+    nl = dims.n_layers
+    _need(q, nl * dims.H * dims.d * _esz(dims), "q")
+    last = ((nl - 1) * kv_layout.layer_stride + (dims.G - 1) * kv_layout.group_stride
+            + (n_tokens - 1) * kv_layout.token_stride + dims.d)
+    _need(k, last * _esz(dims), "k")
+    _need(v, last * _esz(dims), "v")
+    _need(out, nl * dims.H * dims.d * 4, "out")
+    _need(ws, decode_workspace_bytes(dims, n_tokens), "ws")
+    _check("starkv_decode", lib().starkv_decode(
+        ctypes.byref(dims), _ptr(q), _ptr(k), _ptr(v), ctypes.byref(kv_layout), n_tokens,
+        _ptr(out), _ptr(ws), ws.numel() * ws.element_size(), _stream(stream)))

@@ -32,7 +32,7 @@ def declared_functions():
 def test_header_symbols_are_exported():
     L = sk.lib()
     names = declared_functions()
-    assert len(names) == 11
+    assert len(names) == 13
     for n in names:
         assert hasattr(L, n), n
     assert set(names) == set(sk.SIGNATURES)
@@ -203,3 +203,25 @@ def test_state_init_rejects():
     assert sk.STATUS[L.starkv_state_init(ctypes.byref(d), None, 10, None)] == "E_NULL"
     assert sk.STATUS[L.starkv_state_init(ctypes.byref(d), FAKE, -1, None)] == "E_STATE"
     assert sk.STATUS[L.starkv_state_init(ctypes.byref(d), FAKE + 4, 1, None)] == "E_ALIGN"
+
+
+def _decode(d, n=1000, q=FAKE, k=FAKE, v=FAKE, out=FAKE, lay=None, ws=FAKE, ws_bytes=1 << 40):
+    lay = lay or sk.KVLayout(4 * 1000 * 128, 1000 * 128, 128)
+    return sk.STATUS[sk.lib().starkv_decode(ctypes.byref(d), q, k, v, ctypes.byref(lay), n,
+                                            out, ws, ws_bytes, None)]
+
+
+def test_decode_validation_and_workspace():
+    d = dims()
+    assert _decode(d, q=None) == "E_NULL"
+    assert _decode(d, n=0) == "E_SHAPE"
+    assert _decode(dims(dtype=sk.F32)) == "E_DTYPE"
+    assert _decode(dims(H=34, G=2)) == "E_SHAPE"          # 17 heads per group > 16
+    assert _decode(d, lay=sk.KVLayout(0, 0, 100)) == "E_SHAPE"
+    assert _decode(d, lay=sk.KVLayout(0, 0, 132)) == "E_ALIGN"
+    assert _decode(d, k=FAKE + 8) == "E_ALIGN"
+    ws = sk.decode_workspace_bytes(d, 2723)
+    # 28 layers x 4 groups, 3 splits of <= 1024 tokens, 7 heads x (d + 2) floats
+    assert ws == (28 * 4 * 3 * 7 * 130 * 4 + 255) // 256 * 256
+    assert _decode(d, n=2723, ws_bytes=ws - 1) == "E_WORKSPACE"
+    assert sk.decode_workspace_bytes(d, 0) == 0

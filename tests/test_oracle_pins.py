@@ -495,3 +495,44 @@ def test_frame_size_change_resets_stability():
     o, st = O.compress_layer(Q2, K2, V2, L2, W2, spans2, 1, 4, p, st)
     np.testing.assert_array_equal(o["phi"], 0.0)
     assert st.m.shape == (2, 15)
+
+
+# ----------------------------------------------- decode over the cache (4.3)
+
+def test_decode_zero_query_averages_values():
+    """q = 0: every logit is 0, so each head returns the mean of its group's
+    value rows."""
+    r = rng(31)
+    K, V = r.standard_normal((2, 9, 8)), r.standard_normal((2, 9, 8))
+    o = O.decode_attention(np.zeros((4, 8)), K, V)
+    np.testing.assert_allclose(o[:2], np.repeat(V[0].mean(0)[None], 2, 0), rtol=1e-14)
+    np.testing.assert_allclose(o[2:], np.repeat(V[1].mean(0)[None], 2, 0), rtol=1e-14)
+
+
+def test_decode_two_tokens_closed_form():
+    """Two tokens: o = sigma(x1 - x2) v1 + (1 - sigma(x1 - x2)) v2 with
+    x = q.k / sqrt(d)."""
+    q = np.array([[1.0, 2.0, 0.0, -1.0]])
+    K = np.array([[[0.5, 0.0, 1.0, 0.0], [0.0, -1.0, 0.0, 2.0]]])
+    V = np.array([[[1.0, 2.0, 3.0, 4.0], [-4.0, 0.0, 1.0, 0.5]]])
+    x1, x2 = 0.5 / 2.0, -4.0 / 2.0
+    w = 1.0 / (1.0 + math.exp(-(x1 - x2)))
+    np.testing.assert_allclose(O.decode_attention(q, K, V)[0], w * V[0, 0] + (1 - w) * V[0, 1],
+                               rtol=1e-14)
+
+
+def test_decode_brute_force_and_token_permutation():
+    """Against scalar loops on a tiny GQA case; permuting the cached tokens
+    (K and V rows together) leaves the output unchanged."""
+    r = rng(32)
+    H, G, n, d = 6, 3, 7, 5
+    q, K, V = r.standard_normal((H, d)), r.standard_normal((G, n, d)), r.standard_normal((G, n, d))
+    o = O.decode_attention(q, K, V)
+    for h in range(H):
+        g = h * G // H
+        x = [sum(q[h, j] * K[g, t, j] for j in range(d)) / math.sqrt(d) for t in range(n)]
+        e = [math.exp(xi) for xi in x]
+        want = [sum(e[t] * V[g, t, j] for t in range(n)) / sum(e) for j in range(d)]
+        np.testing.assert_allclose(o[h], want, rtol=1e-12)
+    perm = r.permutation(n)
+    np.testing.assert_allclose(O.decode_attention(q, K[:, perm], V[:, perm]), o, rtol=1e-13)
