@@ -52,6 +52,10 @@ def parse():
                          "writes 1 GiB (the calibration of the HBM byte counters)")
     ap.add_argument("--no-per-call", action="store_true",
                     help="skip the per-call timing (no roofline; for counter runs)")
+    ap.add_argument("--decode", action="store_true",
+                    help="instead of the stage: decode attention of one new token per head "
+                         "over the stage's compressed cache and over the full cache, at the "
+                         "trajectory's last step")
     ap.add_argument("--per-head", action="store_true",
                     help="a scoring subspace per query head (the MHA-head granularity "
                          "on the GQA model) instead of one per KV group")
@@ -226,6 +230,8 @@ def main():
         print("bench.py: this build runs the compression stage on one GPU only; "
               "a multi-GPU run is not supported (use --gpus 1).", file=sys.stderr)
         sys.exit(2)
+    if args.decode:
+        return decode_bench(args)
     import numpy as np
     import torch
 
@@ -345,6 +351,137 @@ def main():
     print(json.dumps(line), flush=True)
 
 
+def decode_bench(args):
+    """Decode attention (starkv_decode) of one new token per query head, all
+    layers, at the trajectory's last step: over the K'/V' the stage keeps
+    (B + W rows per group) and over the full cache (L rows).  Each is timed
+    as a HIP graph of `reps` back-to-back launches with HIP events; `value`
+    is decoded tokens per second over the compressed cache."""
+    import numpy as np
+    import torch
+
+    from paper_2606_01790_amd import starkv as sk
+    from paper_2606_01790_amd import workload as WL
+    from paper_2606_01790_amd.pipeline import TrajectoryRunner
+
+    spec = WL.SPECS[args.config]
+    params = sk.params_default()
+    if args.config >= 3:
+        params.t_min, params.t_max = 0.95, 1.05
+    s = spec.steps
+    B = spec.budgets(s)[0]
+    nl, H, G, d, W, L = spec.n_layers, spec.H, spec.G, spec.d, spec.W, spec.L(s)
+    log(f"decode on {spec.name}: running the trajectory to step {s} for K'/V'")
+    r = TrajectoryRunner(spec, params)
+    r.reset()
+    for step in range(1, s + 1):
+        r.load_step(step)
+        r.run_step(step, spec.budgets(step)[0])
+    torch.cuda.synchronize()
+    n_c = B + W
+    rng = np.random.default_rng([spec.seed, 4242])
+    q = torch.from_numpy(WL.f32_to_bf16_bits(
+        rng.standard_normal((nl, H, d), dtype=np.float32)).view(np.int16)).to("cuda")
+    out = torch.empty(nl * H * d, dtype=torch.float32, device="cuda")
+    dims = sk.make_dims(nl, H, G, d, L, W, sk.BF16)
+    kc = r.k_out[:nl * G * n_c * d]
+    vc = r.v_out[:nl * G * n_c * d]
+    lay_c = sk.KVLayout(G * n_c * d, n_c * d, d)
+    cases = {"compressed": (kc, vc, lay_c, n_c), "full": (r.K, r.V, r.layout, L)}
+    stream = torch.cuda.current_stream()
+    reps = 20
+    res = {}
+    for name, (k, v, lay, n) in cases.items():
+        ws = torch.empty(sk.decode_workspace_bytes(dims, n), dtype=torch.uint8, device="cuda")
+        fn = lambda k=k, v=v, lay=lay, n=n, ws=ws: sk.decode(dims, q, k, v, lay, n, out, ws)  # noqa: E731
+        for _ in range(args.warmup):
+            fn()
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g):
+            for _ in range(reps):
+                fn()
+        g.replay()
+        torch.cuda.synchronize()
+        e0 = torch.cuda.Event(enable_timing=True)
+        e1 = torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        for _ in range(args.steps):
+            g.replay()
+        e1.record(stream)
+        torch.cuda.synchronize()
+        t = e0.elapsed_time(e1) * 1e-3 / (args.steps * reps)
+        # algorithmic bytes: every K and V row once, q, the output
+        nbytes = nl * (2 * G * n * d * 2 + H * d * 2 + H * d * 4)
+        res[name] = {"tokens": n, "us_per_token": round(t * 1e6, 2),
+                     "achieved_GBs": round(nbytes / t / 1e9, 1),
+                     "attention_mflops_per_token": round(nl * WL.decode_flops(H, n, d) / 1e6, 2)}
+    comp, full = res["compressed"], res["full"]
+    t_c = comp["us_per_token"] * 1e-6
+    cpu = None
+    if not args.no_cpu_baseline:
+        cpu = decode_cpu_baseline(spec, r, q, n_c, args.cpu_seconds)
+    line = {
+        "metric": "decode attention over the compressed cache: generated tokens/s, all layers",
+        "value": round(1.0 / t_c, 1),
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(t_c * 1e3, 5),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {"workload": spec.name + "-decode", "n_layers": nl, "H": H, "G": G, "d": d,
+                   "W": W, "step": s, "B": B, "cache_tokens_full": L,
+                   "cache_tokens_compressed": n_c, "launch": f"hipgraph x{reps}"},
+        "compressed": comp,
+        "full": full,
+        "speedup_vs_full": round(full["us_per_token"] / comp["us_per_token"], 2),
+        "attention_flops_saving": round(1.0 - comp["attention_mflops_per_token"]
+                                        / full["attention_mflops_per_token"], 4),
+        "roofline": {"bound": "hbm", "achieved": comp["achieved_GBs"], "peak": HBM_PEAK_GBS,
+                     "unit": "GB/s", "frac": round(comp["achieved_GBs"] / HBM_PEAK_GBS, 4),
+                     "traffic": None, "kernel": "starkv_decode",
+                     "avg_launch_us": comp["us_per_token"]},
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(line), flush=True)
+
+
+def decode_cpu_baseline(spec, runner, q, n_c, seconds):
+    """The oracle's decode attention on the host, over the same compressed
+    caches, layer after layer until `seconds` of oracle time have run."""
+    import numpy as np
+
+    from oracle import starkv_oracle as O
+    from paper_2606_01790_amd import workload as WL
+
+    nl, H, G, d = spec.n_layers, spec.H, spec.G, spec.d
+    qh = q.cpu().numpy().view(np.uint16).reshape(nl, H, d)
+    import torch
+    kh = runner.k_out[:nl * G * n_c * d].view(torch.int16).cpu().numpy().view(np.uint16)
+    vh = runner.v_out[:nl * G * n_c * d].view(torch.int16).cpu().numpy().view(np.uint16)
+    kh = kh.reshape(nl, G, n_c, d)
+    vh = vh.reshape(nl, G, n_c, d)
+    spent, layers = 0.0, 0
+    while spent < seconds:
+        layer = layers % nl
+        qf = WL.to_float64(qh[layer], "bf16")
+        kf = WL.to_float64(kh[layer], "bf16")
+        vf = WL.to_float64(vh[layer], "bf16")
+        t0 = time.perf_counter()
+        O.decode_attention(qf, kf, vf)
+        spent += time.perf_counter() - t0
+        layers += 1
+    return {"value": round(layers / nl / spent, 1), "unit": "tokens/s", "cores": blas_threads(),
+            "kind": "oracle",
+            "sample": f"{layers} layer decodes over the compressed caches of {spec.name} "
+                      f"(step {spec.steps}, {n_c} tokens per group; {spent:.1f} s of oracle "
+                      f"time, numpy fp64, BLAS threads {blas_threads()}), scaled to all {nl} layers"}
+
+
 # Sources whose kernels the committed traffic figure was measured on.
 TRAFFIC_SOURCES = {
     "starkv_score": ["score_kernels.h", "score.hip", "score_bf16.hip", "device_common.h"],
@@ -381,6 +518,16 @@ def measured_traffic(call, workload):
         return None
 
 
+def blas_threads():
+    try:
+        from threadpoolctl import threadpool_info
+        blas = [i.get("num_threads", 1) for i in threadpool_info()
+                if i.get("user_api") == "blas"]
+        return max(blas) if blas else 1
+    except Exception:
+        return 1
+
+
 def cpu_baseline(spec, params, seconds, per_head=False):
     """The fp64 oracle, untuned, on the host cores: whole trajectories (every
     step, fresh state) of layers 0, 1, 2, ... of the same workload, cycling
@@ -390,13 +537,7 @@ def cpu_baseline(spec, params, seconds, per_head=False):
     from oracle import starkv_oracle as O
     from paper_2606_01790_amd import workload as WL
 
-    try:
-        from threadpoolctl import threadpool_info
-        blas = [i.get("num_threads", 1) for i in threadpool_info()
-                if i.get("user_api") == "blas"]
-        threads = max(blas) if blas else 1
-    except Exception:
-        threads = 1
+    threads = blas_threads()
     op = O.Params(lam=params.lam, n_warmup=params.n_warmup, n_ramp=params.n_ramp,
                   rho_mi=params.rho_mi, tau=params.tau, rho_t=params.rho_t,
                   delta=params.delta, d_min=params.d_min, t_min=params.t_min,

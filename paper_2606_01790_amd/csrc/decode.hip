@@ -221,21 +221,36 @@ __global__ __launch_bounds__(kDecThreads) void decode_split(DecArgs a) {
   }
 }
 
-// o[layer][h] from the split partials of head h, added in split order.
+// o[layer][h] from the split partials of head h, combined in split order.
 template <int D>
 __global__ __launch_bounds__(D) void decode_merge(DecArgs a) {
   const int h = blockIdx.x, layer = blockIdx.y, d = threadIdx.x;
   const int g = h / a.hpg, hl = h % a.hpg;
-  const float* base = a.part + ((size_t)layer * a.G + g) * a.n_split * a.hpg * (D + 2);
-  float M = -INFINITY;
-  for (int s = 0; s < a.n_split; ++s)
-    M = fmaxf(M, base[((size_t)s * a.hpg + hl) * (D + 2) + D]);
-  float L = 0.f, O = 0.f;
-  for (int s = 0; s < a.n_split; ++s) {
-    const float* rec = base + ((size_t)s * a.hpg + hl) * (D + 2);
-    const float f = __builtin_amdgcn_exp2f(rec[D] - M);
-    L += rec[D + 1] * f;
-    O += rec[d] * f;
+  const float* base = a.part + ((size_t)layer * a.G + g) * a.n_split * a.hpg * (D + 2) +
+                      (size_t)hl * (D + 2);
+  const size_t rs = (size_t)a.hpg * (D + 2);   // record stride between splits
+  // one pass with a running max, sixteen splits' loads in flight at a time
+  float M = -INFINITY, L = 0.f, O = 0.f;
+  for (int s0 = 0; s0 < a.n_split; s0 += 16) {
+    float mv[16], lv[16], ov[16];
+#pragma unroll
+    for (int j = 0; j < 16; ++j) {
+      const bool ok = s0 + j < a.n_split;
+      const float* rec = base + (s0 + j) * rs;
+      mv[j] = ok ? rec[D] : -INFINITY;
+      lv[j] = ok ? rec[D + 1] : 0.f;
+      ov[j] = ok ? rec[d] : 0.f;
+    }
+#pragma unroll
+    for (int j = 0; j < 16; ++j) {
+      if (mv[j] == -INFINITY) continue;   // past the last split
+      const float Mn = fmaxf(M, mv[j]);
+      const float fo = M == Mn ? 1.0f : __builtin_amdgcn_exp2f(M - Mn);
+      const float fj = __builtin_amdgcn_exp2f(mv[j] - Mn);
+      L = L * fo + lv[j] * fj;
+      O = O * fo + ov[j] * fj;
+      M = Mn;
+    }
   }
   a.out[((size_t)layer * a.H + h) * D + d] = O / L;
 }

@@ -150,9 +150,10 @@ starkv_status check_decode(const starkv_dims* dims, int32_t n_tokens, DecodeGeom
     g->G = (int)G;
     g->d = (int)d;
     g->n_tok = n_tokens;
-    // about 1024 tokens per block, at most ~2048 blocks in all
-    const int64_t cap = std::max<int64_t>(1, 2048 / (nl * G));
-    int64_t ns = std::min<int64_t>((n_tokens + 1023) / 1024, cap);
+    // about 256 tokens (two tiles per wave) per block, at most ~4096 blocks:
+    // enough blocks in flight to cover the HBM latency of a short cache
+    const int64_t cap = std::max<int64_t>(1, 4096 / (nl * G));
+    int64_t ns = std::min<int64_t>((n_tokens + 255) / 256, cap);
     int64_t chunk = (n_tokens + ns - 1) / ns;
     chunk = (chunk + 31) / 32 * 32;
     g->chunk = (int)chunk;

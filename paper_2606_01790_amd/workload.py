@@ -313,3 +313,9 @@ def bytes_alg(spec: WorkloadSpec, step: int, B: int) -> int:
 def qk_flops(H: int, W: int, L_p: int, d: int) -> int:
     """Flops of the window-query/key contraction, counted once: 2 H W L_p d."""
     return 2 * H * W * L_p * d
+
+
+def decode_flops(H: int, n: int, d: int) -> int:
+    """Attention flops of one decoded token in one layer over n cached tokens:
+    q.K and p.V, 2 H n d each."""
+    return 4 * H * n * d

@@ -221,7 +221,7 @@ def test_decode_validation_and_workspace():
     assert _decode(d, lay=sk.KVLayout(0, 0, 132)) == "E_ALIGN"
     assert _decode(d, k=FAKE + 8) == "E_ALIGN"
     ws = sk.decode_workspace_bytes(d, 2723)
-    # 28 layers x 4 groups, 3 splits of <= 1024 tokens, 7 heads x (d + 2) floats
-    assert ws == (28 * 4 * 3 * 7 * 130 * 4 + 255) // 256 * 256
+    # 28 layers x 4 groups, 11 splits of <= 256 tokens, 7 heads x (d + 2) floats
+    assert ws == (28 * 4 * 11 * 7 * 130 * 4 + 255) // 256 * 256
     assert _decode(d, n=2723, ws_bytes=ws - 1) == "E_WORKSPACE"
     assert sk.decode_workspace_bytes(d, 0) == 0
