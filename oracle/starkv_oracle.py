@@ -45,6 +45,8 @@ class Params:
     grid: int = 8             # M x M spatial grid (paper silent; reading)
     pool_kernel: int = 5      # AvgPool1D width (paper silent; reading)
     eps: float = 1e-8         # the paper's epsilon (value unstated; reading)
+    tem_decay: str = "exp"    # TEM decay: "exp" (the paper's), "linear", "gamma"
+    aeb_mode: str = "entropy"  # AEB statistic: "entropy" (the paper's), "confidence"
 
 
 @dataclass
@@ -248,14 +250,33 @@ def stability(s_cur: np.ndarray, m: np.ndarray, rho_t: float, eps: float):
 
 def temporal_discount(is_vis: np.ndarray, frame: np.ndarray, F: int,
                       phi_of_token: np.ndarray, delta: float,
-                      d_min: float) -> np.ndarray:
+                      d_min: float, decay: str = "exp") -> np.ndarray:
     """D_t = D_min + (1 - D_min) exp(-eta_t), eta_t = delta * Delta_f(t) *
     phi_{g*(t)} for historical visual tokens, D_t = 1 otherwise (sec. 3.5),
-    with the frame distance Delta_f(t) = F - f(t) of sec. 3.1."""
+    with the frame distance Delta_f(t) = F - f(t) of sec. 3.1.
+
+    The decay ablation (sec. 4.2, temporal weighting functions) compares the
+    exponential with a linear and a gamma decay but does not write them out.
+    Readings, both with D = 1 at Delta_f = 0 or phi = 0, the floor D_min and
+    the exponential's slope at the origin:
+      linear: D_min + (1 - D_min) max(0, 1 - eta), reaching the floor at
+              eta = 1 (it lies below the exponential: the paper finds it
+              discards history too aggressively);
+      gamma:  D_min + (1 - D_min) (1 + Delta_f)^(-delta phi), a power law of
+              the frame distance (it lies above the exponential: the paper
+              finds it keeps more long-range history)."""
     D = np.ones(is_vis.shape[0], dtype=np.float64)
     dist = (F - frame).astype(np.float64)
     eta = delta * dist * phi_of_token
-    D_vis = d_min + (1.0 - d_min) * np.exp(-eta)
+    if decay == "exp":
+        f = np.exp(-eta)
+    elif decay == "linear":
+        f = np.maximum(0.0, 1.0 - eta)
+    elif decay == "gamma":
+        f = np.power(1.0 + dist, -delta * phi_of_token)
+    else:
+        raise ValueError(decay)
+    D_vis = d_min + (1.0 - d_min) * f
     D[is_vis] = D_vis[is_vis]
     return D
 
@@ -284,6 +305,36 @@ def entropy_temperature(sbar: np.ndarray, t_min: float, t_max: float,
         h_hat = min(1.0, max(0.0, h_hat))
     T = t_min + (t_max - t_min) * h_hat
     return h_hat, T
+
+
+def confidence_temperature(sbar: np.ndarray, t_min: float, t_max: float,
+                           eps: float):
+    """The confidence-based AEB of the ablation (sec. 4.2, entropy- vs
+    confidence-based AEB): the temperature comes from the peak mass p_max of
+    the base distribution instead of its entropy.  The paper gives no formula;
+    reading: p_t = sbar_t / (sum sbar + eps), the confidence
+    c = (p_max - 1/L_p) / (1 - 1/L_p) clamped to [0, 1] (0 for a uniform,
+    1 for a one-hot distribution; 1 for a single token), and
+    T = T_min + (T_max - T_min) (1 - c), so that both ends meet the entropy
+    variant's.  Returns (1 - c, T): the statistic in the place of H^."""
+    L_p = sbar.shape[0]
+    p = sbar / (sbar.sum() + eps)
+    if L_p <= 1:
+        c = 1.0
+    else:
+        c = (float(p.max()) - 1.0 / L_p) / (1.0 - 1.0 / L_p)
+        c = min(1.0, max(0.0, c))
+    u = 1.0 - c
+    return u, t_min + (t_max - t_min) * u
+
+
+def aeb_temperature(sbar: np.ndarray, params: "Params"):
+    """The AEB statistic in [0, 1] and T for the configured variant."""
+    if params.aeb_mode == "confidence":
+        return confidence_temperature(sbar, params.t_min, params.t_max, params.eps)
+    if params.aeb_mode != "entropy":
+        raise ValueError(params.aeb_mode)
+    return entropy_temperature(sbar, params.t_min, params.t_max, params.eps)
 
 
 # --------------------------------------------------------------------------
@@ -400,10 +451,10 @@ def compress_layer(Q, K, V, L: int, W: int, spans, F: int, B: int,
         phi, m_new = stability(s_cur, m_old, p.rho_t, p.eps)
     else:
         phi, m_new = np.zeros(G, dtype=np.float64), state.m.copy()
-    D = temporal_discount(is_vis, frame, F, phi[gstar], p.delta, p.d_min)
+    D = temporal_discount(is_vis, frame, F, phi[gstar], p.delta, p.d_min, p.tem_decay)
 
     # AEB (sec. 3.6)
-    h_hat, T = entropy_temperature(sbar, p.t_min, p.t_max, p.eps)
+    h_hat, T = aeb_temperature(sbar, p)
 
     # Fusion and selection (sec. 3.2, 3.7)
     s_f, s = final_score(sbar, beta, D, T)

@@ -536,3 +536,56 @@ def test_decode_brute_force_and_token_permutation():
         np.testing.assert_allclose(o[h], want, rtol=1e-12)
     perm = r.permutation(n)
     np.testing.assert_allclose(O.decode_attention(q, K[:, perm], V[:, perm]), o, rtol=1e-13)
+
+
+# --------------------------------- ablation variants (sec. 4.2, readings)
+
+def _disc(decay, dist, phi, delta=0.2, d_min=0.1):
+    n = len(dist)
+    return O.temporal_discount(np.ones(n, bool), 10 - np.asarray(dist, float), 10,
+                               np.asarray(phi, float), delta, d_min, decay)
+
+
+@pytest.mark.parametrize("decay", ["exp", "linear", "gamma"])
+def test_decay_variants_shared_properties(decay):
+    """Every decay: D = 1 for the current frame or phi = 0, D in [D_min, 1],
+    non-increasing in the frame distance, and the exponential's slope at 0."""
+    assert np.all(_disc(decay, [0, 0], [0.7, 1.0]) == 1.0)
+    assert np.all(_disc(decay, [3, 9], [0.0, 0.0]) == 1.0)
+    D = _disc(decay, np.arange(0, 60), np.full(60, 0.9))
+    assert np.all((D >= 0.1) & (D <= 1.0)) and np.all(np.diff(D) <= 0)
+    h = 1e-6     # one-sided derivative in the frame distance at 0, phi = 0.5
+    d1 = _disc(decay, np.array([h]), [0.5])[0]
+    assert (1.0 - d1) / (h * 0.2 * 0.5) == pytest.approx(0.9, rel=1e-4)
+
+
+def test_decay_variant_closed_forms_and_order():
+    """Linear: D_min + (1 - D_min)(1 - eta), floored at D_min from eta = 1;
+    gamma: D_min + (1 - D_min)(1 + dist)^(-delta phi).  For every distance
+    linear <= exponential <= gamma (1 - x <= e^-x <= (1 + d)^(-c) with
+    x = c d): the ablation's finding that linear drops history hardest and
+    gamma keeps the most."""
+    np.testing.assert_allclose(_disc("linear", [2], [1.0]), [0.1 + 0.9 * 0.6], rtol=1e-15)
+    np.testing.assert_allclose(_disc("linear", [6], [1.0]), [0.1], rtol=1e-15)
+    np.testing.assert_allclose(_disc("gamma", [3], [0.5]), [0.1 + 0.9 * 4 ** -0.1], rtol=1e-14)
+    dist, phi = np.arange(1, 40), np.linspace(0.05, 1.0, 39)
+    lin, ex, ga = (_disc(k, dist, phi) for k in ("linear", "exp", "gamma"))
+    assert np.all(lin <= ex + 1e-15) and np.all(ex <= ga + 1e-15)
+
+
+def test_confidence_temperature_ends_and_scale_invariance():
+    """Uniform base scores: confidence 0, T = T_max (as the entropy variant);
+    one-hot: confidence 1, T = T_min; a single token counts as one-hot; the
+    statistic does not change when sbar is scaled."""
+    u, T = O.confidence_temperature(np.full(50, 0.3), 0.75, 1.25, 0.0)
+    assert u == pytest.approx(1.0, abs=1e-12) and T == pytest.approx(1.25, abs=1e-12)
+    x = np.zeros(50)
+    x[7] = 2.0
+    u, T = O.confidence_temperature(x, 0.75, 1.25, 0.0)
+    assert u == pytest.approx(0.0, abs=1e-12) and T == pytest.approx(0.75, abs=1e-12)
+    assert O.confidence_temperature(np.array([3.0]), 0.75, 1.25, 1e-8) == (0.0, 0.75)
+    r = rng(41).random(300)
+    a, b = O.confidence_temperature(r, 0.9, 1.1, 0.0), O.confidence_temperature(r * 7.0, 0.9, 1.1, 0.0)
+    assert a[0] == pytest.approx(b[0], rel=1e-12)
+    p = r / r.sum()
+    assert a[0] == pytest.approx(1.0 - (p.max() - 1 / 300) / (1 - 1 / 300), rel=1e-12)
