@@ -56,6 +56,10 @@ def parse():
                     help="instead of the stage: decode attention of one new token per head "
                          "over the stage's compressed cache and over the full cache, at the "
                          "trajectory's last step")
+    ap.add_argument("--tem-decay", choices=["exp", "linear", "gamma"], default="exp",
+                    help="temporal discount variant of the decay ablation (exp is the paper's)")
+    ap.add_argument("--aeb", choices=["entropy", "confidence"], default="entropy",
+                    help="AEB temperature variant of the ablation (entropy is the paper's)")
     ap.add_argument("--per-head", action="store_true",
                     help="a scoring subspace per query head (the MHA-head granularity "
                          "on the GQA model) instead of one per KV group")
@@ -243,10 +247,13 @@ def main():
     params = sk.params_default()
     if args.config >= 3:
         params.t_min, params.t_max = 0.95, 1.05
+    params.tem_decay, params.aeb_mode = sk.TEM_DECAY[args.tem_decay], sk.AEB_MODE[args.aeb]
     log(f"workload {spec.name}: building resident inputs")
     n_states = args.warmup + 3
     wl = Workload(spec, params, n_states, per_head=args.per_head)
-    workload = spec.name + ("-per-head" if args.per_head else "")
+    workload = (spec.name + ("-per-head" if args.per_head else "")
+                + ("" if args.tem_decay == "exp" else f"-tem-{args.tem_decay}")
+                + ("" if args.aeb == "entropy" else f"-aeb-{args.aeb}"))
     layer_tokens = spec.n_layers * sum(spec.n_vis(s) for s in range(1, spec.steps + 1))
     bytes_alg = spec.n_layers * sum(WL.bytes_alg(spec, s, spec.budgets(s)[0])
                                     for s in range(1, spec.steps + 1))
@@ -311,7 +318,8 @@ def main():
 
     cpu = None
     if not args.no_cpu_baseline:
-        cpu = cpu_baseline(spec, params, args.cpu_seconds, args.per_head)
+        cpu = cpu_baseline(spec, params, args.cpu_seconds, args.per_head, args.tem_decay,
+                           args.aeb)
 
     line = {
         "metric": METRIC,
@@ -528,7 +536,7 @@ def blas_threads():
         return 1
 
 
-def cpu_baseline(spec, params, seconds, per_head=False):
+def cpu_baseline(spec, params, seconds, per_head=False, tem_decay="exp", aeb="entropy"):
     """The fp64 oracle, untuned, on the host cores: whole trajectories (every
     step, fresh state) of layers 0, 1, 2, ... of the same workload, cycling
     through the layers again if needed, until `seconds` of oracle time have
@@ -542,7 +550,8 @@ def cpu_baseline(spec, params, seconds, per_head=False):
                   rho_mi=params.rho_mi, tau=params.tau, rho_t=params.rho_t,
                   delta=params.delta, d_min=params.d_min, t_min=params.t_min,
                   t_max=params.t_max, n_bins=params.n_bins, grid=params.grid,
-                  pool_kernel=params.pool_kernel, eps=params.eps)
+                  pool_kernel=params.pool_kernel, eps=params.eps, tem_decay=tem_decay,
+                  aeb_mode=aeb)
     tr = WL.Trajectory(spec)
     log(f"cpu baseline: oracle trajectories until {seconds:.0f} s of oracle time")
     spent, tokens, runs, layer = 0.0, 0, 0, 0

@@ -121,7 +121,34 @@ typedef struct starkv_params {
   int32_t grid;       /* M x M spatial grid, [1, 16]                          (8) */
   int32_t pool_kernel;/* odd AvgPool1D width, [1, 63]                         (5) */
   float eps;          /* the paper's epsilon, >= 0                         (1e-8) */
+  /* Ablation variants (sec. 4.2); the paper does not write their formulas,
+   * the readings are given with the enums. */
+  int32_t tem_decay;  /* starkv_tem_decay of the temporal discount  (EXP) */
+  int32_t aeb_mode;   /* starkv_aeb_mode of the AEB temperature  (ENTROPY) */
 } starkv_params;
+
+/* Temporal discount D_t of historical visual tokens (sec. 3.5), with
+ * eta = delta * (F - f(t)) * phi_{g*(t)}:
+ *   EXP     D_min + (1 - D_min) exp(-eta)                 (the paper's)
+ *   LINEAR  D_min + (1 - D_min) max(0, 1 - eta)
+ *   GAMMA   D_min + (1 - D_min) (1 + F - f(t))^(-delta * phi_{g*(t)})
+ * All three are 1 at distance 0 or phi = 0, floor at D_min and share the
+ * exponential's slope at distance 0; linear lies below it, gamma above. */
+typedef enum starkv_tem_decay {
+  STARKV_TEM_EXP = 0,
+  STARKV_TEM_LINEAR = 1,
+  STARKV_TEM_GAMMA = 2
+} starkv_tem_decay;
+
+/* Statistic u in [0, 1] behind the AEB temperature T = t_min + (t_max -
+ * t_min) u (sec. 3.6), with p = sbar / (sum sbar + eps) over the L_p tokens:
+ *   ENTROPY     u = H^ = -sum p ln(p + eps) / ln L_p, clamped   (the paper's)
+ *   CONFIDENCE  u = 1 - c, c = (max p - 1/L_p) / (1 - 1/L_p) clamped to
+ *               [0, 1] (c = 1 for L_p = 1): the peak-mass variant. */
+typedef enum starkv_aeb_mode {
+  STARKV_AEB_ENTROPY = 0,
+  STARKV_AEB_CONFIDENCE = 1
+} starkv_aeb_mode;
 
 /* A visual span (sec. 3.1): rows*cols visual tokens of one screenshot, laid
  * out row-major from token `start` (token start + r*cols + c has screen
@@ -143,7 +170,7 @@ typedef struct starkv_span {
  *   [2G, 3G)   prior weights w_g                  (sec. 3.4)
  *   [3G, 4G)   stability phi_g                    (sec. 3.5)
  *   4G         lambda_eff of this step
- *   4G+1       normalised entropy H^              (sec. 3.6)
+ *   4G+1       AEB statistic u: H^, or 1 - c      (sec. 3.6, starkv_aeb_mode)
  *   4G+2       temperature T
  *   4G+3       step count n (as a float)                                    */
 #define STARKV_SCAL_MI(G) 0
@@ -220,7 +247,8 @@ starkv_status starkv_score(const starkv_dims* dims, const starkv_params* params,
  *   phi_g   = cos(S[g, current frame], m_g) (eps in the denominator), then
  *             m_g = rho_t*m_g + (1-rho_t)*S[g, current frame]; m_g restarts
  *             from 0 when the current frame's token count changes;
- *   H^      = clamp(-sum p ln(p+eps) / ln L_p, 0, 1), p = sbar/(sum sbar + eps);
+ *   H^      = clamp(-sum p ln(p+eps) / ln L_p, 0, 1), p = sbar/(sum sbar + eps)
+ *             (or the params->aeb_mode variant, see starkv_aeb_mode);
  *   T       = t_min + (t_max - t_min) * H^.
  * S, sbar: device, as written by starkv_score.
  * spans:   host, n_spans in [0, STARKV_MAX_SPANS]; frame: the current
@@ -242,7 +270,7 @@ starkv_status starkv_update_state(const starkv_dims* dims,
  * discount, sec. 3.7 selection; Algorithm 1, fusion and selection lines):
  *   beta_t = (1 - lambda_eff) + lambda_eff * Ns * w[gstar_t],
  *   D_t    = d_min + (1 - d_min) exp(-delta (F - f(t)) phi[gstar_t]) on visual
- *            tokens, 1 elsewhere,
+ *            tokens (or the params->tem_decay variant), 1 elsewhere,
  *   s_t    = max(sbar_t beta_t D_t, 0)^(1/T) (no power when 1/T == 1),
  *   idx    = the B tokens of largest s (lower index first on ties), ascending.
  * sbar, gstar: device, from starkv_score; scalars: device, from

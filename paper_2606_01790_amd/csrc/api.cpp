@@ -57,6 +57,8 @@ void starkv_params_default(starkv_params* p) {
   p->grid = 8;
   p->pool_kernel = 5;
   p->eps = 1e-8f;
+  p->tem_decay = STARKV_TEM_EXP;
+  p->aeb_mode = STARKV_AEB_ENTROPY;
 }
 
 size_t starkv_workspace_bytes(const starkv_dims* dims) {

@@ -34,6 +34,7 @@ struct SelArgs {
   int32_t* idx;
   int G, Lp, B, sc, frame, cache;
   float delta, d_min;
+  int tem;              // starkv_tem_decay
   int n_spans;
   int32_t start[STARKV_MAX_SPANS];
   int32_t end[STARKV_MAX_SPANS];
@@ -46,6 +47,7 @@ __global__ __launch_bounds__(kThreads) void select_kernel(SelArgs a) {
   __shared__ __align__(16) uint32_t cand[kCand];
   __shared__ int sp_start[STARKV_MAX_SPANS], sp_end[STARKV_MAX_SPANS];
   __shared__ float sp_dist[STARKV_MAX_SPANS];
+  __shared__ float sp_ldist[STARKV_MAX_SPANS];   // log2(1 + distance), gamma decay
   __shared__ int sh_cnt[kWaves];
   __shared__ int n_cand;
   __shared__ float w_s[STARKV_MAX_GROUPS], phi_s[STARKV_MAX_GROUPS];
@@ -68,6 +70,7 @@ __global__ __launch_bounds__(kThreads) void select_kernel(SelArgs a) {
     sp_start[tid] = a.start[tid];
     sp_end[tid] = a.end[tid];
     sp_dist[tid] = (float)(a.frame - a.sframe[tid]);
+    sp_ldist[tid] = __log2f(1.0f + sp_dist[tid]);
   }
   __syncthreads();
   const float lam = scal[STARKV_SCAL_LAMBDA(a.G)];
@@ -95,8 +98,14 @@ __global__ __launch_bounds__(kThreads) void select_kernel(SelArgs a) {
         const float beta = (1.0f - lam) + gl * w_s[g];
         float D = 1.0f;
         while (cur < a.n_spans && sp_end[cur] <= t) ++cur;
-        if (cur < a.n_spans && sp_start[cur] <= t)
-          D = a.d_min + (1.0f - a.d_min) * __expf(-a.delta * sp_dist[cur] * phi_s[g]);
+        if (cur < a.n_spans && sp_start[cur] <= t) {
+          const float dp = a.delta * phi_s[g];
+          float f;
+          if (a.tem == STARKV_TEM_EXP) f = __expf(-a.delta * sp_dist[cur] * phi_s[g]);
+          else if (a.tem == STARKV_TEM_LINEAR) f = fmaxf(0.0f, 1.0f - dp * sp_dist[cur]);
+          else f = exp2f(-dp * sp_ldist[cur]);
+          D = a.d_min + (1.0f - a.d_min) * f;
+        }
         const float sf = fmaxf(sbv[u] * beta * D, 0.0f);
         const float sv = (inv_t == 1.0f || sf == 0.0f) ? sf : exp2f(inv_t * __log2f(sf));
         s_out[t] = sv;
@@ -305,6 +314,7 @@ int launch_select(const Geometry& g, const starkv_params& p, const float* sbar,
   a.cache = g.Lp < kLdsKeys ? g.Lp : kLdsKeys;
   a.delta = p.delta;
   a.d_min = p.d_min;
+  a.tem = p.tem_decay;
   a.n_spans = n_spans;
   for (int i = 0; i < n_spans; ++i) {
     a.start[i] = spans[i].start;

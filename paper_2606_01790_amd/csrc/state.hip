@@ -50,6 +50,7 @@ struct StatsArgs {
   size_t state_stride;
   size_t m_off;
   int G, Lp, nbins, grid, cur, frame_cap, sc;
+  int aeb;                // starkv_aeb_mode
   float rho_t, eps;
   SpanSet sp;
   FinalArgs fin;          // the layer's finalize, run by its last block
@@ -108,6 +109,7 @@ __device__ void stats_body(const StatsArgs& a) {
   if (g == a.G) {   // ------------------------------------ entropy block
     const float* sb = a.sbar + (size_t)layer * a.Lp;
     double z = 0.0;
+    float vmax = 0.f;     // s-bar is non-negative
     for (int t0 = tid; t0 < a.Lp; t0 += kBatch * kThreads) {
       float v[kBatch];
 #pragma unroll
@@ -116,10 +118,30 @@ __device__ void stats_body(const StatsArgs& a) {
         v[u] = t < a.Lp ? sb[t] : 0.f;
       }
 #pragma unroll
-      for (int u = 0; u < kBatch; ++u) z += (double)v[u];
+      for (int u = 0; u < kBatch; ++u) {
+        z += (double)v[u];
+        vmax = fmaxf(vmax, v[u]);
+      }
     }
     z = block_sum_d(z, red);
     const double denom = z + (double)a.eps;
+    if (a.aeb == STARKV_AEB_CONFIDENCE) {   // peak-mass variant: u = 1 - c
+      vmax = wave_max(vmax);
+      __shared__ float red_max[kWaves];
+      if (lane == 0) red_max[wave] = vmax;
+      __syncthreads();
+      if (tid == 0) {
+        float m = 0.f;
+        for (int w = 0; w < kWaves; ++w) m = fmaxf(m, red_max[w]);
+        double c = 1.0;
+        if (a.Lp > 1) {
+          const double inv = 1.0 / (double)a.Lp;
+          c = fmin(1.0, fmax(0.0, ((double)m / denom - inv) / (1.0 - inv)));
+        }
+        scal[STARKV_SCAL_HHAT(a.G)] = (float)(1.0 - c);
+      }
+      return;
+    }
     double e = 0.0;
     for (int t0 = tid; t0 < a.Lp; t0 += kBatch * kThreads) {
       float v[kBatch];
@@ -753,6 +775,7 @@ int launch_update_state(const Geometry& g, const starkv_params& p,
   a.cur = current_span(spans, n_spans, frame);
   a.frame_cap = frame_cap;
   a.sc = (int)scalars_count(g.Ns);
+  a.aeb = p.aeb_mode;
   a.rho_t = p.rho_t;
   a.eps = p.eps;
   a.sp.n = n_spans;

@@ -77,6 +77,9 @@ starkv_status check_params(const starkv_params* p) {
   if (p->n_bins < 1 || p->n_bins > 64) return STARKV_E_PARAM;
   if (p->grid < 1 || p->grid > 16) return STARKV_E_PARAM;
   if (!finite(p->eps) || p->eps < 0.f) return STARKV_E_PARAM;
+  if (p->tem_decay < STARKV_TEM_EXP || p->tem_decay > STARKV_TEM_GAMMA) return STARKV_E_PARAM;
+  if (p->aeb_mode < STARKV_AEB_ENTROPY || p->aeb_mode > STARKV_AEB_CONFIDENCE)
+    return STARKV_E_PARAM;
   return check_pool(p);
 }
 

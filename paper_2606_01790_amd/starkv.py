@@ -19,6 +19,8 @@ LIB_PATH = os.path.join(_PKG, "libstarkv.so")
 
 F32 = 0
 BF16 = 1
+TEM_DECAY = {"exp": 0, "linear": 1, "gamma": 2}     # starkv_tem_decay
+AEB_MODE = {"entropy": 0, "confidence": 1}          # starkv_aeb_mode
 MAX_SPANS = 64
 
 STATUS = {
@@ -53,7 +55,8 @@ class Params(ctypes.Structure):
                 ("rho_mi", c_float), ("tau", c_float), ("rho_t", c_float),
                 ("delta", c_float), ("d_min", c_float), ("t_min", c_float),
                 ("t_max", c_float), ("n_bins", c_int32), ("grid", c_int32),
-                ("pool_kernel", c_int32), ("eps", c_float)]
+                ("pool_kernel", c_int32), ("eps", c_float), ("tem_decay", c_int32),
+                ("aeb_mode", c_int32)]
 
 
 class Span(ctypes.Structure):

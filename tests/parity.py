@@ -30,7 +30,9 @@ def oracle_params(p: sk.Params) -> O.Params:
                     rho_mi=float(p.rho_mi), tau=float(p.tau), rho_t=float(p.rho_t),
                     delta=float(p.delta), d_min=float(p.d_min), t_min=float(p.t_min),
                     t_max=float(p.t_max), n_bins=int(p.n_bins), grid=int(p.grid),
-                    pool_kernel=int(p.pool_kernel), eps=float(p.eps))
+                    pool_kernel=int(p.pool_kernel), eps=float(p.eps),
+                    tem_decay={v: k for k, v in sk.TEM_DECAY.items()}[int(p.tem_decay)],
+                    aeb_mode={v: k for k, v in sk.AEB_MODE.items()}[int(p.aeb_mode)])
 
 
 def max_rel(a, b):
@@ -90,7 +92,7 @@ def check_layer(tag, K, V, L, W, spans, F, B, op: O.Params, G, gpu: dict,
     assert np.max(np.abs(f["mi"] - mi_stage)) <= 1e-5, f"{tag}: MI stage {f['mi']} vs {mi_stage}"
     w_stage = O.mi_prior(f["mi_bar"].astype(np.float64), op.tau, op.eps)
     assert np.max(np.abs(f["w"] - w_stage)) <= 1e-5, f"{tag}: w stage"
-    h_stage, T_stage = O.entropy_temperature(sbar_g, op.t_min, op.t_max, op.eps)
+    h_stage, T_stage = O.aeb_temperature(sbar_g, op)
     assert abs(f["h_hat"] - h_stage) <= 1e-5 and abs(f["T"] - T_stage) <= 1e-5, f"{tag}: H/T stage"
 
     # ---- online statistics, end to end
@@ -104,7 +106,7 @@ def check_layer(tag, K, V, L, W, spans, F, B, op: O.Params, G, gpu: dict,
     lam = float(f["lam"])
     beta = (1.0 - lam) + lam * G * f["w"].astype(np.float64)[gst_g]
     D = O.temporal_discount(is_vis, frame, F, f["phi"].astype(np.float64)[gst_g],
-                            op.delta, op.d_min)
+                            op.delta, op.d_min, op.tem_decay)
     _, s_stage = O.final_score(sbar_g, beta, D, float(f["T"]))
     r_s_stage = max_rel(s_g, s_stage)
     assert r_s_stage <= 1e-4, f"{tag}: s stage rel {r_s_stage}"

@@ -154,6 +154,15 @@ def _update(d, spans, frame, p=None, cap=2691):
         FAKE, None, 0, None)]
 
 
+def test_variant_params_are_validated():
+    d = dims()
+    for field, bad in (("tem_decay", 3), ("tem_decay", -1), ("aeb_mode", 2)):
+        p = sk.params_default()
+        assert (p.tem_decay, p.aeb_mode) == (0, 0)
+        setattr(p, field, bad)
+        assert _update(d, [(0, 39, 69, 1)], 1, p=p) == "E_PARAM"
+
+
 def test_update_state_rejects_bad_spans_and_params():
     d = dims(L=2947)                         # L_p = 2915
     ok = [(0, 39, 69, 1)]

@@ -52,13 +52,15 @@ class HostFrames:
 
 
 def run_trajectory(cid, layers=None, prior_active=False, steps=None, groups=1,
-                   per_head=False, on_step=None):
+                   per_head=False, on_step=None, tem_decay="exp", aeb_mode="entropy"):
     """per_head: a subspace per query head; the oracle then scores the cache
     with every shared K group replicated across its heads."""
     spec = WL.SPECS[cid]
     p = params_for(cid, prior_active)
+    p.tem_decay, p.aeb_mode = sk.TEM_DECAY[tem_decay], sk.AEB_MODE[aeb_mode]
     op = oracle_params(p)
-    say(f"cfg{cid} prior_active={prior_active} per_head={per_head}: allocate")
+    say(f"cfg{cid} prior_active={prior_active} per_head={per_head} tem={tem_decay} "
+        f"aeb={aeb_mode}: allocate")
     runner = TrajectoryRunner(spec, p, per_head=per_head)
     runner.reset()
     host = HostFrames(spec)
@@ -411,3 +413,20 @@ def test_config6_image_slots_and_resolution_change():
             assert np.all(phi > 0.0), f"step {step}: phi {phi[:2]}"
 
     run_trajectory(6, layers=[0, 1, 27], prior_active=True, on_step=on_step)
+
+
+# ------------------------------------------- ablation variants (sec. 4.2)
+
+@pytest.mark.parametrize("tem,aeb", [("linear", "entropy"), ("gamma", "confidence"),
+                                     ("exp", "confidence")])
+def test_ablation_variants_trajectory(tem, aeb):
+    """The linear and gamma temporal decays and the confidence-based AEB on
+    the 28-layer trajectory (discount active from step 2, prior active),
+    layers 0 and 27, against the oracle with the same readings."""
+    run_trajectory(3, layers=[0, 27], prior_active=True, tem_decay=tem, aeb_mode=aeb)
+
+
+def test_confidence_aeb_single_frame():
+    """One 1920x1080 frame with the single-image T range [0.75, 1.25]: the
+    temperature comes from the peak base-score mass."""
+    run_trajectory(2, prior_active=True, aeb_mode="confidence")
