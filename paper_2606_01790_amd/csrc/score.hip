@@ -99,12 +99,11 @@ int launch_score(const Geometry& g, const starkv_params& p, const void* q,
   const float inv_norm = 1.0f / ((float)p.pool_kernel * (float)g.hps);
   dim3 ag((g.Lp + 255) / 256, g.n_layers);
   const size_t lds = (size_t)g.Ns * (256 + 2 * radius) * sizeof(float);
-  static bool configured = false;   // one-time, idempotent
-  if (!configured) {
-    hipFuncSetAttribute(reinterpret_cast<const void*>(&score_aggregate),
-                        hipFuncAttributeMaxDynamicSharedMemorySize, 160 * 1024);
-    configured = true;
-  }
+  // once per process; function-local static initialisation is thread-safe
+  static const hipError_t attr = hipFuncSetAttribute(
+      reinterpret_cast<const void*>(&score_aggregate), hipFuncAttributeMaxDynamicSharedMemorySize,
+      160 * 1024);
+  (void)attr;
   score_aggregate<<<ag, 256, lds, st>>>(a.sraw, S, sbar, gstar, g.Ns, g.Lp, radius,
                                         inv_norm, 1.0f / (float)g.Ns);
   return (int)hipGetLastError();

@@ -322,13 +322,11 @@ int launch_select(const Geometry& g, const starkv_params& p, const float* sbar,
     a.sframe[i] = spans[i].frame;
   }
   const size_t lds = (size_t)a.cache * sizeof(uint32_t);
-  static bool configured = false;   // one-time, idempotent
-  if (!configured) {
-    hipFuncSetAttribute(reinterpret_cast<const void*>(&select_kernel),
-                        hipFuncAttributeMaxDynamicSharedMemorySize,
-                        (int)(kLdsKeys * sizeof(uint32_t)));
-    configured = true;
-  }
+  // once per process; function-local static initialisation is thread-safe
+  static const hipError_t attr = hipFuncSetAttribute(
+      reinterpret_cast<const void*>(&select_kernel), hipFuncAttributeMaxDynamicSharedMemorySize,
+      (int)(kLdsKeys * sizeof(uint32_t)));
+  (void)attr;
   select_kernel<<<g.n_layers, kThreads, lds, st>>>(a);
   return (int)hipGetLastError();
 }

@@ -787,12 +787,11 @@ int launch_update_state(const Geometry& g, const starkv_params& p,
     a.sp.frame[i] = spans[i].frame;
     a.sp.off[i + 1] = a.sp.off[i] + spans[i].rows * spans[i].cols;
   }
-  static bool configured = false;   // one-time, idempotent
-  if (!configured) {
-    hipFuncSetAttribute(reinterpret_cast<const void*>(&stats_kernel),
-                        hipFuncAttributeMaxDynamicSharedMemorySize, (int)kStatsLds);
-    configured = true;
-  }
+  // once per process; function-local static initialisation is thread-safe
+  static const hipError_t attr = hipFuncSetAttribute(
+      reinterpret_cast<const void*>(&stats_kernel), hipFuncAttributeMaxDynamicSharedMemorySize,
+      (int)kStatsLds);
+  (void)attr;
   FinalArgs& f = a.fin;
   f.scal = scalars;
   f.state = a.state;
