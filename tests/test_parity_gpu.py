@@ -430,3 +430,29 @@ def test_confidence_aeb_single_frame():
     """One 1920x1080 frame with the single-image T range [0.75, 1.25]: the
     temperature comes from the peak base-score mass."""
     run_trajectory(2, prior_active=True, aeb_mode="confidence")
+
+
+# ------------------------------------------------ largest shapes, no spans
+
+def test_largest_window_row_block_bf16():
+    """R = W * H / G = 512 window rows per group (16 MFMA row blocks, the
+    largest accepted; d = 64 so that the rows fit the 128 KiB row budget)."""
+    p = params_for(2, prior_active=True)
+    spans = [(40, 18, 24, 1)]
+    run_case("R=512", 32, 2, 64, 32, 900, spans, 1, 120, "bf16", p, seed=61, n_layers=1)
+
+
+def test_largest_window_row_block_f32():
+    """R = 128 window rows in fp32 (four row blocks, the fp32 maximum)."""
+    p = params_for(2, prior_active=True)
+    spans = [(0, 10, 20, 1)]
+    run_case("R=128 f32", 8, 2, 64, 32, 400, spans, 1, 60, "f32", p, seed=62, n_layers=1)
+
+
+def test_no_visual_spans():
+    """A text-only cache: no visual token, so MI = 0 and phi = 0 in every
+    group, D = 1, and the selection runs on s-bar alone."""
+    p = params_for(2, prior_active=True)
+    _, states = run_case("no spans", 8, 2, 64, 8, 500, [], 0, 80, "bf16", p, seed=63)
+    for st in states:
+        assert np.all(st.mi_bar == 0.0)
