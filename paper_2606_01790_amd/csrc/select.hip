@@ -1,14 +1,16 @@
 // Final score and global top-B (Eq. final_score, sec. 3.2; sec. 3.5 discount;
 // sec. 3.7 selection).  One 1024-thread workgroup per layer:
-//   1. s_t = max(sbar_t * beta_t * D_t, 0)^(1/T) for every past token,
+//   1. s_t = max(sbar_t * beta_t * D_t, 0)^(1/T) for every past token
+//      (D_t with the configured decay: exponential, linear or gamma),
 //      written out and kept as a descending-order key in LDS (the span of a
 //      token comes from an LDS copy of the span table, walked by a cursor
 //      since each thread's tokens ascend);
 //   2. MSB-first radix select of the B-th key in the order (s descending,
 //      token index ascending): the bits every key shares are skipped, the
 //      first digit is 12 bits wide (one histogram, block-wide scan); the keys
-//      in the cut's bucket are then compacted into LDS when they fit and the
-//      later 8-bit digits count only those;
+//      in the cut's bucket are then compacted into LDS when they fit: at most
+//      256 of them rank themselves directly, more are finished by 8-bit
+//      digits counting only those;
 //   3. ordered compaction: each wave owns a contiguous token segment, counts
 //      its selected tokens (keys past the cut, plus the lowest-index ties at
 //      the cut) with ballots, and writes them at its segment's offset, so idx

@@ -1,23 +1,30 @@
 // Online statistics of one step (sec. 3.4-3.6).
 //
-// stats kernel, grid (G + 2, n_layers), 1024 threads:
-//   block g < G   spatial MI of group g (sec. 3.4, Eq. MI);
-//   block G       normalised entropy H^ of sbar (sec. 3.6);
-//   block G + 1   stability phi_g of every group with the stability-mean
+// stats kernel, grid (G + 2, n_layers), 1024 threads, where G is the call's
+// number of scoring subspaces (the KV groups, or the query heads):
+//   block g < G   spatial MI of subspace g (sec. 3.4, Eq. MI);
+//   block G       the AEB statistic of sbar: normalised entropy H^ (sec. 3.6),
+//                 or one minus the normalised peak mass in the confidence
+//                 variant;
+//   block G + 1   stability phi_g of every subspace with the stability-mean
 //                 update (sec. 3.5).
 // The last block of each layer to finish then runs the layer's finalize in
 // one wave: MI EMA, min-max prior w, lambda schedule, temperature T, state
 // bookkeeping.
 //
-// Equal-frequency binning ranks the visual tokens of a group by (value,
+// Equal-frequency binning ranks the visual tokens of a subspace by (value,
 // token index).  The bin edges are the K-1 order statistics at ranks
 // ceil(b N / K), found together by one MSB-first radix select over
-// order-preserving 32-bit keys: the bits every key shares are skipped, the
-// first digit is 12 bits wide (one LDS histogram, block-wide scan), later
-// digits are 8 bits with one histogram per distinct edge prefix and one
-// wave scanning per edge.  A token's bin is the number of edges at or below
-// it; equal keys at an edge are split by token index with an ordered block
-// scan, so ties resolve exactly as the ranking defines.
+// order-preserving 32-bit keys: the bits every key shares are skipped and
+// the first digit is 12 bits wide (one LDS histogram, block-wide scan).
+// When few keys (<= 256) share the edges' first-digit buckets, the joint
+// histogram pass itself bins every other key (its bin is the number of edges
+// in lower buckets) and collects the few, which are then ranked directly and
+// binned exactly.  Otherwise those keys are compacted into per-bucket
+// segments, later 8-bit digits (one histogram per distinct edge prefix, one
+// wave per edge) finish the edges, and the joint histogram pass bins every
+// key by comparison, splitting equal keys at an edge by token index with an
+// ordered block scan, so ties resolve exactly as the ranking defines.
 #include "device_common.h"
 #include "internal.h"
 
