@@ -4,8 +4,9 @@
 // The window softmax of every query row needs that row's max and sum over
 // all L_p past keys before any key's normalised mass is known, so scoring
 // runs in two passes over K:
-//   pass 1  per (layer, group, token chunk): for each window row r, the
-//           chunk's max M_r and sum of 2^(y - M_r), y = q.k * log2(e)/sqrt(d);
+//   pass 1  per (layer, group, token chunk): for each window row r, a
+//           reference M_r no larger than the chunk's max and the sum of
+//           2^(y - M_r), y = q.k * log2(e)/sqrt(d);
 //   pass 2  merges the chunk statistics into c_r = M_r + log2(l_r) (every
 //           block for its own group) and sums 2^(y_rt - c_r) over the
 //           group's rows for every token t.
@@ -174,7 +175,12 @@ __global__ __launch_bounds__(NRB * 64) void score_pass1(ScoreArgs a) {
   STARKV_STAGE_STORE(KS, NRB * 64, sr, kbuf)
   __syncthreads();
 
-  float m = kNegBig, l = 0.f;
+  // (m, l): reference logit and sum of 2^((y - m) * log2e/sqrt(d)) of the
+  // lane's row over the tokens seen so far.  Any reference gives the same
+  // statistics once merged, so m is not the running max: it is moved only
+  // when a block's sum would leave [0, 2^32), i.e. before the first block
+  // and when logits rise well above it.
+  float m = kNegBig, ms = kNegBig * a.scale, l = 0.f;
   // MFMA chain of one 32-token block: acc[4i+j] = token 32b + 8i + 4*half + j,
   // query row wave*32 + l32
   auto chain = [&](const T* tile, int b) {
@@ -185,6 +191,21 @@ __global__ __launch_bounds__(NRB * 64) void score_pass1(ScoreArgs a) {
     return acc;
   };
   auto epilogue = [&](f32x16& acc, int tb, bool full) {
+    if (full) {
+      // against the kept reference: no max and no rescale.  With no
+      // reference yet (m = -1e30) the sum is +inf; a sum of 2^32 or more
+      // means the block's logits exceed m by more than 18 log2 units (l
+      // counts at most 2^14 tokens of mass <= 1 otherwise).  Both, and a NaN,
+      // redo the block below against the block's exact max.
+      float sum = __builtin_amdgcn_exp2f(fmaf(acc[0], a.scale, -ms));
+#pragma unroll
+      for (int e = 1; e < 16; ++e) sum += __builtin_amdgcn_exp2f(fmaf(acc[e], a.scale, -ms));
+      const float ln = l + sum;
+      if (ln < 4294967296.0f) {
+        l = ln;
+        return;
+      }
+    }
     float mt;
     if (full) {
       mt = acc[0];
@@ -200,12 +221,13 @@ __global__ __launch_bounds__(NRB * 64) void score_pass1(ScoreArgs a) {
       }
     }
     const float mn = fmaxf(m, mt);
-    const float ms = mn * a.scale;
-    float sum = 0.f;
+    const float msn = mn * a.scale;
+    float sum = __builtin_amdgcn_exp2f(fmaf(acc[0], a.scale, -msn));
 #pragma unroll
-    for (int e = 0; e < 16; ++e) sum += __builtin_amdgcn_exp2f(fmaf(acc[e], a.scale, -ms));
-    l = l * rescale(m, mn, ms, a.scale) + sum;
+    for (int e = 1; e < 16; ++e) sum += __builtin_amdgcn_exp2f(fmaf(acc[e], a.scale, -msn));
+    l = l * rescale(m, mn, msn, a.scale) + sum;
     m = mn;
+    ms = msn;
   };
   int buf = 0;
   for (int t0 = t_begin; t0 < t_end; t0 += KS::kRows) {
@@ -239,11 +261,11 @@ __global__ __launch_bounds__(NRB * 64) void score_pass1(ScoreArgs a) {
   // the two lane halves hold the same query row over other tokens
   const float mo = other_half(m, half), lo = other_half(l, half);
   const float mn = fmaxf(m, mo);
-  const float ms = mn * a.scale;
-  l = l * rescale(m, mn, ms, a.scale) + lo * rescale(mo, mn, ms, a.scale);
+  const float msn = mn * a.scale;
+  l = l * rescale(m, mn, msn, a.scale) + lo * rescale(mo, mn, msn, a.scale);
   if (half == 0) {
     float2* out = a.part + ((size_t)(layer * a.G + g) * a.n_chunks_max + chunk) * a.Rpad;
-    out[wave * 32 + l32] = make_float2(mn * a.scale, l);
+    out[wave * 32 + l32] = make_float2(msn, l);
   }
 }
 
@@ -337,18 +359,18 @@ __global__ __launch_bounds__(NRB * 64) void score_pass2(ScoreArgs a) {
       // reads); both halves then hold the same sum and store it to the same
       // address
       if (n_part == 1) {
-        float v = 0.f;
+        float v = __builtin_amdgcn_exp2f(fmaf(acc[0], a.scale, -c[0]));
 #pragma unroll
-        for (int e = 0; e < 16; ++e) v += __builtin_amdgcn_exp2f(fmaf(acc[e], a.scale, -c[e]));
+        for (int e = 1; e < 16; ++e) v += __builtin_amdgcn_exp2f(fmaf(acc[e], a.scale, -c[e]));
         v += other_half(v, half);
         rs[wave * KS::kRows + 32 * b + l32] = v;
       } else {
         // one partial per 8-row group: rows 8i + 4*half + (0..3) here
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
-          float v = 0.f;
+          float v = __builtin_amdgcn_exp2f(fmaf(acc[4 * i], a.scale, -c[4 * i]));
 #pragma unroll
-          for (int j = 0; j < 4; ++j)
+          for (int j = 1; j < 4; ++j)
             v += __builtin_amdgcn_exp2f(fmaf(acc[4 * i + j], a.scale, -c[4 * i + j]));
           rs[(wave * 4 + i) * KS::kRows + 32 * b + l32] = v + other_half(v, half);
         }

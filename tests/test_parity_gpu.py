@@ -328,6 +328,38 @@ def test_exact_ties_everywhere():
     run_case("ties", H, G, d, W, L, spans, 1, 50, "bf16", p, Qs=Qs, Ks=Ks, Vs=Vs)
 
 
+@pytest.mark.parametrize("dtype,d,H,G,W", [("bf16", 128, 28, 4, 32), ("f32", 64, 16, 2, 16)])
+def test_rising_and_spiking_logits(dtype, d, H, G, W):
+    """Pass 1 keeps a row's reference logit until a block's sum would leave
+    [0, 2^32).  Layer 0: keys scaled up along the token index, so the logits
+    of most rows keep rising within every chunk.  Layer 1: spike keys equal
+    to s times one window query (s = 2, 4, 12), whose logit for that row sits
+    about 30, 65 and 200 log2 units above the rest: the last overflows the
+    block sum to +inf.  Spikes fall in the first block, mid-chunk, on a tile
+    edge and on the last past token."""
+    p = params_for(2, prior_active=True)
+    L = 3000 + W
+    Lp = L - W
+    Qs, Ks, Vs = WL.random_case(12, 2, H, G, d, L, W, dtype)
+    Qf = WL.to_float64(Qs, dtype).astype(np.float32)
+    Kf = WL.to_float64(Ks, dtype).astype(np.float32)
+    ramp = (1.0 + 3.0 * np.arange(L, dtype=np.float32) / L)[:, None]
+    Kf[0] *= ramp[None]
+    hpg = H // G
+    for i, (t, s) in enumerate([(5, 12.0), (300, 2.0), (767, 4.0), (1024, 12.0),
+                                (1535, 2.0), (2000, 4.0), (Lp - 1, 12.0)]):
+        for g in range(G):
+            h = g * hpg + (i + g) % hpg
+            Kf[1, g, t] = s * Qf[1, h, (t + g) % W]
+    if dtype == "bf16":
+        Ks = WL.f32_to_bf16_bits(Kf)
+    else:
+        Ks = Kf
+    spans = [(0, 40, 60, 1), (2400, 20, 30, 2)]
+    run_case(f"rising {dtype}", H, G, d, W, L, spans, 2, 400, dtype, p, Qs=Qs, Ks=Ks,
+             Vs=Vs)
+
+
 def test_frame_size_change_resets_stability():
     """Two steps whose current frames differ in size: m_g restarts, phi = 0."""
     p = params_for(3, prior_active=True)
