@@ -70,6 +70,7 @@ constexpr int kHistInts = 16384;          // 64 KiB: digit or joint histograms
 constexpr int kKeyCache = 20 * 1024;      // visual keys kept in LDS
 constexpr int kCand = 2048;               // keys in the edges' first-digit buckets
 constexpr int kDirect = 256;              // candidates ranked directly, no more digits
+constexpr int kJointOff = 8192;           // joint histogram slot when digits follow
 constexpr size_t kStatsLds =
     (size_t)kHistInts * 4 + (size_t)kKeyCache * 4 + (size_t)kCand * 4;
 
@@ -83,7 +84,7 @@ __device__ inline int scaled_index(int x, int M, int n, float m_over_n) {
   return q;
 }
 
-__device__ void stats_body(const StatsArgs& a) {
+__device__ __forceinline__ void stats_body(const StatsArgs& a) {
   extern __shared__ __align__(16) unsigned char smem[];
   int* hist = reinterpret_cast<int*>(smem);
   uint32_t* kc = reinterpret_cast<uint32_t*>(smem + (size_t)kHistInts * 4);
@@ -100,7 +101,8 @@ __device__ void stats_body(const StatsArgs& a) {
   __shared__ uint32_t seg_dg[64];         // distinct edge buckets, ascending
   __shared__ int seg_off[64], seg_cnt[64], seg_cur[64];
   __shared__ int n_seg;
-  __shared__ uint32_t cand_v[kDirect];    // fused pass: cell << 24 | visual index
+  __shared__ int sp_start[STARKV_MAX_SPANS], sp_rows[STARKV_MAX_SPANS];
+  __shared__ int sp_cols[STARKV_MAX_SPANS], sp_off[STARKV_MAX_SPANS + 1];
   __shared__ int nb_s[64];
   __shared__ int nc_s[256];
   __shared__ int sh_cnt[kWaves];
@@ -243,31 +245,90 @@ __device__ void stats_body(const StatsArgs& a) {
   const int N = a.sp.off[a.sp.n];
   const int K = a.nbins;
   const int M = a.grid;
+  const int ncell = M * M;
   const bool cached = N <= kKeyCache;
+  // Candidates (keys in the edges' first-digit buckets): the fused pass
+  // keeps (key, cell << 24 | visual index) pairs, the compaction pass keys
+  // only; in the candidate area while the keys are cached, else in the key
+  // cache.
+  uint32_t* ck = cached ? cand : kc;
+  const int fcap = cached ? kCand / 2 : kKeyCache / 2;
+  const int ccap = cached ? kCand : kKeyCache;
+  uint32_t* cv = ck + fcap;
+  // joint (bin, cell) histogram: at the start of hist, or past the digit
+  // histograms when the fused pass fills it before the last digits
+  int* jh = hist;
   double mi = 0.0;
 
   if (N > 0) {
+    // span table to LDS (a uniform index keeps the argument in scalar loads)
+    if (tid == 0) {
+      for (int s = 0; s < a.sp.n; ++s) {
+        sp_off[s] = a.sp.off[s];
+        sp_start[s] = a.sp.start[s];
+        sp_rows[s] = a.sp.rows[s];
+        sp_cols[s] = a.sp.cols[s];
+      }
+      sp_off[a.sp.n] = N;
+    }
+    __syncthreads();
+    // Visual index i (ascending per thread) -> its span, by a cursor s.
+    auto span_of = [&](int s, int i) {
+      while (sp_off[s + 1] <= i) ++s;
+      return s;
+    };
+    // The kBatch keys i0 + u * kThreads of this thread (0 past N), read from
+    // S with kBatch loads in flight.  Returns the advanced cursor.
+    auto fetch = [&](int i0, int s, uint32_t (&kv)[kBatch]) {
+      float v[kBatch];
+#pragma unroll
+      for (int u = 0; u < kBatch; ++u) {
+        const int i = i0 + u * kThreads;
+        v[u] = 0.f;
+        if (i < N) {
+          s = span_of(s, i);
+          v[u] = Sg[sp_start[s] + (i - sp_off[s])];
+        }
+      }
+#pragma unroll
+      for (int u = 0; u < kBatch; ++u) kv[u] = i0 + u * kThreads < N ? fkey(v[u]) : 0u;
+      return s;
+    };
+    // the same from the key cache, or from S when the keys are not cached
+    auto keys = [&](int i0, int s, uint32_t (&kv)[kBatch]) {
+      if (!cached) return fetch(i0, s, kv);
+#pragma unroll
+      for (int u = 0; u < kBatch; ++u) {
+        const int i = i0 + u * kThreads;
+        kv[u] = i < N ? kc[i] : 0u;
+      }
+      return s;
+    };
+    // grid cell of visual index i in span s
+    auto cell_of = [&](int s, int i) {
+      const int p = i - sp_off[s], cols = sp_cols[s], rows = sp_rows[s];
+      int r = (int)((float)p * (1.0f / (float)cols));
+      if (r * cols > p) --r;
+      else if ((r + 1) * cols <= p) ++r;
+      const int c = p - r * cols;
+      return scaled_index(r, M, rows, (float)M / (float)rows) * M +
+             scaled_index(c, M, cols, (float)M / (float)cols);
+    };
+
     // ---- visual keys (LDS when they fit), min and max
     uint32_t lo = 0xFFFFFFFFu, hi = 0u;
-    for (int s = 0; s < a.sp.n; ++s) {
-      const int n_s = a.sp.rows[s] * a.sp.cols[s];
-      const float* src = Sg + a.sp.start[s];
-      uint32_t* dst = kc + a.sp.off[s];
-      for (int i0 = tid; i0 < n_s; i0 += kBatch * kThreads) {
-        float v[kBatch];
-#pragma unroll
-        for (int u = 0; u < kBatch; ++u) {   // kBatch loads in flight
-          const int i = i0 + u * kThreads;
-          v[u] = i < n_s ? src[i] : 0.f;
-        }
+    {
+      int s = 0;
+      for (int i0 = tid; i0 < N; i0 += kBatch * kThreads) {
+        uint32_t kv[kBatch];
+        s = fetch(i0, s, kv);
 #pragma unroll
         for (int u = 0; u < kBatch; ++u) {
           const int i = i0 + u * kThreads;
-          if (i < n_s) {
-            const uint32_t k = fkey(v[u]);
-            if (cached) dst[i] = k;
-            lo = min(lo, k);
-            hi = max(hi, k);
+          if (i < N) {
+            if (cached) kc[i] = kv[u];
+            lo = min(lo, kv[u]);
+            hi = max(hi, kv[u]);
           }
         }
       }
@@ -293,17 +354,30 @@ __device__ void stats_body(const StatsArgs& a) {
     // ---- multi-target radix select: a 12-bit first digit (one histogram,
     // every target shares the common prefix), then 8-bit digits with one
     // histogram per distinct prefix.  After the first digit the keys in the
-    // edges' buckets are compacted into LDS when they fit, and the later
-    // digits scan only those.
+    // edges' buckets are kept in LDS when they fit, and the later digits scan
+    // only those: the fused pass keeps them while it bins every other key
+    // into the joint histogram; otherwise a compaction pass keeps their keys.
     bool first = true, compact = false, fused = false;
     int n_c = 0, f_shift = 0, f_nb = 1;
-    // Few candidates, compacted into one segment per edge bucket: each ranks
-    // itself among its bucket's keys; the one whose rank range holds an
-    // edge's rank is that edge's key.  Leaves the exact edges in t_*.
+    // first-digit buckets of the edges (valid once the first digit is known)
+    uint32_t eb[8];
+    auto lower_edges = [&](uint32_t d) {
+      int n = 0;
+      if (n_t <= 8) {
+#pragma unroll
+        for (int j = 0; j < 8; ++j) n += eb[j] < d;
+      } else {
+        for (int b = 0; b < n_t; ++b) n += ((t_key[b] >> f_shift) & (uint32_t)(f_nb - 1)) < d;
+      }
+      return n;
+    };
+    // Few candidates, in one segment per edge bucket: each ranks itself
+    // among its bucket's keys; the one whose rank range holds an edge's rank
+    // is that edge's key.  Leaves the exact edges in t_*.
     auto direct_rank = [&](int shift) {
       const int ns = n_seg;
       if (tid < n_c) {
-        const uint32_t key = cand[tid];
+        const uint32_t key = ck[tid];
         const uint32_t pre = key_hi(key, shift);
         int sg = 0;
         while (sg + 1 < ns && seg_off[sg + 1] <= tid) ++sg;
@@ -312,7 +386,7 @@ __device__ void stats_body(const StatsArgs& a) {
         for (int j0 = seg_off[sg]; j0 < j_end; j0 += 4) {
           uint32_t kv[4];
 #pragma unroll
-          for (int u = 0; u < 4; ++u) kv[u] = cand[min(j0 + u, j_end - 1)];
+          for (int u = 0; u < 4; ++u) kv[u] = ck[min(j0 + u, j_end - 1)];
 #pragma unroll
           for (int u = 0; u < 4; ++u) {
             const bool in = j0 + u < j_end;
@@ -336,6 +410,24 @@ __device__ void stats_body(const StatsArgs& a) {
         t_eq[tid] = n_eq[tid];
       }
       __syncthreads();
+    };
+    // segment of candidate slot j (segments are contiguous and ascending)
+    auto seg_of = [&](int j) {
+      int lo_s = 0, hi_s = n_seg - 1;
+      while (lo_s < hi_s) {
+        const int mid = (lo_s + hi_s + 1) >> 1;
+        if (seg_off[mid] <= j) lo_s = mid; else hi_s = mid - 1;
+      }
+      return lo_s;
+    };
+    // segment of first-digit bucket d, which holds an edge
+    auto seg_of_bucket = [&](uint32_t d) {
+      int lo_s = 0, hi_s = n_seg - 1;
+      while (lo_s < hi_s) {
+        const int mid = (lo_s + hi_s) >> 1;
+        if (seg_dg[mid] < d) lo_s = mid + 1; else hi_s = mid;
+      }
+      return lo_s;
     };
     for (int done = common; done < 32;) {
       const int width = min(first ? 12 : 8, 32 - done);
@@ -374,14 +466,15 @@ __device__ void stats_body(const StatsArgs& a) {
             if (i0 + u * kThreads < N) atomicAdd(&hist[(kv[u] >> shift) & (nb - 1)], 1);
         }
       } else if (compact) {
-        for (int i = tid; i < n_c; i += kThreads) count(cand[i]);
-      } else if (cached) {
-        for (int i = tid; i < N; i += kThreads) count(kc[i]);
+        for (int i = tid; i < n_c; i += kThreads) count(ck[i]);
       } else {
-        for (int s = 0; s < a.sp.n; ++s) {
-          const int n_s = a.sp.rows[s] * a.sp.cols[s];
-          const float* src = Sg + a.sp.start[s];
-          for (int i = tid; i < n_s; i += kThreads) count(fkey(src[i]));
+        int s = 0;
+        for (int i0 = tid; i0 < N; i0 += kBatch * kThreads) {
+          uint32_t kv[kBatch];
+          s = keys(i0, s, kv);
+#pragma unroll
+          for (int u = 0; u < kBatch; ++u)
+            if (i0 + u * kThreads < N) count(kv[u]);
         }
       }
       __syncthreads();
@@ -438,42 +531,63 @@ __device__ void stats_body(const StatsArgs& a) {
           if (lane == 63) { cand_total = inc; n_seg = slot + 1; }
         }
         __syncthreads();
-        if (cand_total <= kDirect && K * M * M <= kHistInts && N < (1 << 24)) {
-          // few keys share the edges' buckets: the joint histogram pass
-          // below also collects them, and they are binned once the edges
-          // are exact
+        if (cand_total <= fcap && (K - 1) * 256 <= kJointOff &&
+            kJointOff + K * ncell <= kHistInts && N < (1 << 24)) {
+          // ---- fused pass: every key outside the edges' buckets goes to
+          // the joint histogram (its bin is the number of edges in lower
+          // buckets); the others are kept with their cell and visual index
           fused = true;
           f_shift = shift;
           f_nb = nb;
-          n_c = cand_total;
-          done = 32 - width;
-        } else if (done + width < 32 && cand_total <= kCand) {
-          // compact them, each bucket's keys in its own segment (in any
-          // order inside it)
-          const int ns = n_seg;
-          auto keep = [&](uint32_t key, bool valid) {
-            const uint32_t dg = (key >> shift) & (uint32_t)(nb - 1);
-            if (valid && ((bucket_bits[dg >> 5] >> (dg & 31)) & 1u)) {
-              int lo = 0, hi = ns - 1;
-              while (lo < hi) {
-                const int mid = (lo + hi) >> 1;
-                if (seg_dg[mid] < dg) lo = mid + 1; else hi = mid;
+          jh = hist + kJointOff;
+          for (int i = tid; i < K * ncell; i += kThreads) jh[i] = 0;
+#pragma unroll
+          for (int j = 0; j < 8; ++j)
+            eb[j] = j < n_t ? ((t_key[j] >> shift) & (uint32_t)(nb - 1)) : 0xFFFFFFFFu;
+          __syncthreads();
+          int s = 0, sc = 0;
+          for (int i0 = tid; i0 < N; i0 += kBatch * kThreads) {
+            uint32_t kv[kBatch];
+            s = keys(i0, s, kv);
+#pragma unroll
+            for (int u = 0; u < kBatch; ++u) {
+              const int i = i0 + u * kThreads;
+              if (i < N) {
+                const uint32_t key = kv[u];
+                const uint32_t d = (key >> shift) & (uint32_t)(nb - 1);
+                sc = span_of(sc, i);
+                const int cell = cell_of(sc, i);
+                if ((bucket_bits[d >> 5] >> (d & 31)) & 1u) {
+                  const int sg = seg_of_bucket(d);
+                  const int pos = seg_off[sg] + atomicAdd(&seg_cur[sg], 1);
+                  ck[pos] = key;
+                  cv[pos] = ((uint32_t)cell << 24) | (uint32_t)i;
+                } else {
+                  atomicAdd(&jh[lower_edges(d) * ncell + cell], 1);
+                }
               }
-              cand[seg_off[lo] + atomicAdd(&seg_cur[lo], 1)] = key;
             }
-          };
-          if (cached) {
-            for (int i0 = 0; i0 < N; i0 += kThreads) {
-              const int i = i0 + tid;
-              keep(i < N ? kc[i] : 0u, i < N);
-            }
-          } else {
-            for (int s = 0; s < a.sp.n; ++s) {
-              const int n_s = a.sp.rows[s] * a.sp.cols[s];
-              const float* src = Sg + a.sp.start[s];
-              for (int i0 = 0; i0 < n_s; i0 += kThreads) {
-                const int i = i0 + tid;
-                keep(i < n_s ? fkey(src[i]) : 0u, i < n_s);
+          }
+          __syncthreads();
+          compact = true;
+          n_c = cand_total;
+          if (n_c <= kDirect) {
+            direct_rank(shift);
+            done = 32 - width;   // every edge is exact: no more digits
+          }
+        } else if (done + width < 32 && cand_total <= ccap) {
+          // compaction: each bucket's keys in its own segment (in any order
+          // inside it)
+          int s = 0;
+          for (int i0 = tid; i0 < N; i0 += kBatch * kThreads) {
+            uint32_t kv[kBatch];
+            s = keys(i0, s, kv);
+#pragma unroll
+            for (int u = 0; u < kBatch; ++u) {
+              const uint32_t dg = (kv[u] >> shift) & (uint32_t)(nb - 1);
+              if (i0 + u * kThreads < N && ((bucket_bits[dg >> 5] >> (dg & 31)) & 1u)) {
+                const int sg = seg_of_bucket(dg);
+                ck[seg_off[sg] + atomicAdd(&seg_cur[sg], 1)] = kv[u];
               }
             }
           }
@@ -501,70 +615,16 @@ __device__ void stats_body(const StatsArgs& a) {
       first = false;
     }
 
-    const int ncell = M * M;
     if (fused) {
-      // ---- joint histogram of the tokens outside the edges' buckets (their
-      // bin is the count of edges in lower buckets); the others are kept
-      // with their visual index
-      for (int i = tid; i < K * ncell; i += kThreads) hist[i] = 0;
-      uint32_t eb[8];
-#pragma unroll
-      for (int j = 0; j < 8; ++j)
-        eb[j] = j < n_t ? ((t_key[j] >> f_shift) & (uint32_t)(f_nb - 1)) : 0xFFFFFFFFu;
-      auto lower_edges = [&](uint32_t d) {
-        int n = 0;
-        if (n_t <= 8) {
-#pragma unroll
-          for (int j = 0; j < 8; ++j) n += eb[j] < d;
-        } else {
-          for (int b = 0; b < n_t; ++b) n += ((t_key[b] >> f_shift) & (uint32_t)(f_nb - 1)) < d;
-        }
-        return n;
-      };
-      __syncthreads();
-      const int ns = n_seg;
-      for (int s = 0; s < a.sp.n; ++s) {
-        const int rows = a.sp.rows[s], cols = a.sp.cols[s];
-        const int n_s = rows * cols;
-        const uint32_t* kcs = kc + a.sp.off[s];
-        const float* src = Sg + a.sp.start[s];
-        const float fr = (float)M / (float)rows, fc = (float)M / (float)cols;
-        int r = tid / cols, c = tid - (tid / cols) * cols;
-        const int dq = kThreads / cols, dr = kThreads - dq * cols;
-        for (int i0 = 0; i0 < n_s; i0 += kThreads) {
-          const int i = i0 + tid;
-          if (i < n_s) {
-            const uint32_t key = cached ? kcs[i] : fkey(src[i]);
-            const uint32_t d = (key >> f_shift) & (uint32_t)(f_nb - 1);
-            const int cell = scaled_index(r, M, rows, fr) * M + scaled_index(c, M, cols, fc);
-            if ((bucket_bits[d >> 5] >> (d & 31)) & 1u) {
-              int lo = 0, hi = ns - 1;
-              while (lo < hi) {
-                const int mid = (lo + hi) >> 1;
-                if (seg_dg[mid] < d) lo = mid + 1; else hi = mid;
-              }
-              const int pos = seg_off[lo] + atomicAdd(&seg_cur[lo], 1);
-              cand[pos] = key;
-              cand_v[pos] = ((uint32_t)cell << 24) | (uint32_t)(a.sp.off[s] + i);
-            } else {
-              atomicAdd(&hist[lower_edges(d) * ncell + cell], 1);
-            }
-          }
-          c += dr;
-          r += dq;
-          if (c >= cols) { c -= cols; ++r; }
-        }
-      }
-      __syncthreads();
-      direct_rank(f_shift);
-      // ---- the kept tokens: equal keys at an edge split by visual index
-      if (tid < n_c) {
-        const uint32_t key = cand[tid];
-        const uint32_t v = cand_v[tid] & 0xFFFFFFu;
-        const int cell = (int)(cand_v[tid] >> 24);
+      // ---- the kept tokens, now that the edges are exact: a key above an
+      // edge of its bucket is past it; equal keys at an edge split by
+      // visual index (the ranking's tie rule)
+      for (int j = tid; j < n_c; j += kThreads) {
+        const uint32_t key = ck[j];
+        const uint32_t v = cv[j] & 0xFFFFFFu;
+        const int cell = (int)(cv[j] >> 24);
         const uint32_t d = (key >> f_shift) & (uint32_t)(f_nb - 1);
-        int sg = 0;
-        while (sg + 1 < ns && seg_off[sg + 1] <= tid) ++sg;
+        const int sg = seg_of(j);
         const int j0 = seg_off[sg], j_end = j0 + seg_cnt[sg];
         int bin = lower_edges(d);
         for (int b = 0; b < n_t; ++b) {
@@ -577,88 +637,82 @@ __device__ void stats_body(const StatsArgs& a) {
               ++bin;       // the edge's own token, the only one with its key
             } else {
               int pos = 0;   // equal keys before this token in visual order
-              for (int j = j0; j < j_end; ++j) pos += cand[j] == key && (cand_v[j] & 0xFFFFFFu) < v;
+              for (int jj = j0; jj < j_end; ++jj) pos += ck[jj] == key && (cv[jj] & 0xFFFFFFu) < v;
               bin += pos >= t_rank[b];
             }
           }
         }
-        atomicAdd(&hist[bin * ncell + cell], 1);
+        atomicAdd(&jh[bin * ncell + cell], 1);
       }
       __syncthreads();
     } else {
-    // ---- joint histogram of (bin, cell), spans in order, row-major inside
-    // a span (the visual-token order the ranking's tie rule refers to)
-    for (int i = tid; i < K * ncell; i += kThreads) hist[i] = 0;
-    bool any_tie = false;
-    for (int b = 0; b < n_t; ++b) any_tie |= (t_eq[b] > 1);
-    if (tid < 64) carry_s[tid] = 0;
-    uint32_t tk[8];
+      // ---- joint histogram of (bin, cell) in visual-token order (the order
+      // the ranking's tie rule refers to): block-wide batches of kThreads
+      // consecutive tokens
+      for (int i = tid; i < K * ncell; i += kThreads) hist[i] = 0;
+      bool any_tie = false;
+      for (int b = 0; b < n_t; ++b) any_tie |= (t_eq[b] > 1);
+      if (tid < 64) carry_s[tid] = 0;
+      uint32_t tk[8];
 #pragma unroll
-    for (int j = 0; j < 8; ++j) tk[j] = j < n_t ? t_key[j] : 0u;
-    __syncthreads();
-    for (int s = 0; s < a.sp.n; ++s) {
-      const int rows = a.sp.rows[s], cols = a.sp.cols[s];
-      const int n_s = rows * cols;
-      const uint32_t* kcs = kc + a.sp.off[s];
-      const float* src = Sg + a.sp.start[s];
-      const float fr = (float)M / (float)rows, fc = (float)M / (float)cols;
-      // (row, col) of token i0 + tid, advanced by kThreads per iteration
-      int r = tid / cols, c = tid - (tid / cols) * cols;
-      const int dq = kThreads / cols, dr = kThreads - dq * cols;
-      for (int i0 = 0; i0 < n_s; i0 += kThreads) {
-        const int i = i0 + tid;
-        const bool valid = i < n_s;
-        const uint32_t key = valid ? (cached ? kcs[i] : fkey(src[i])) : 0u;
-        int bin = 0;
-        if (!any_tie) {
-          if (n_t <= 8) {
+      for (int j = 0; j < 8; ++j) tk[j] = j < n_t ? t_key[j] : 0u;
+      __syncthreads();
+      int s = 0, sc = 0;
+      for (int i0 = 0; i0 < N; i0 += kBatch * kThreads) {
+        uint32_t kv[kBatch];
+        s = keys(i0 + tid, s, kv);
 #pragma unroll
-            for (int j = 0; j < 8; ++j) bin += (j < n_t) & (key >= tk[j]);
-          } else {
-            for (int b = 0; b < n_t; ++b) bin += (key >= t_key[b]);
-          }
-        } else {
-          for (int b = 0; b < n_t; ++b) {
-            if (t_eq[b] > 1) {   // uniform branch: ordered split of equal keys
-              const bool eq = valid && (key == t_key[b]);
-              const int c0 = carry_s[b];
-              int tot;
-              const int pos = block_excl_count(eq, sh_cnt, &tot) + c0;
-              bin += (key > t_key[b]) || (eq && pos >= t_rank[b]);
-              __syncthreads();
-              if (tid == 0) carry_s[b] = c0 + tot;
-              __syncthreads();
+        for (int u = 0; u < kBatch; ++u) {
+          const int i = i0 + u * kThreads + tid;
+          const bool valid = i < N;
+          const uint32_t key = kv[u];
+          int bin = 0;
+          if (!any_tie) {
+            if (n_t <= 8) {
+#pragma unroll
+              for (int j = 0; j < 8; ++j) bin += (j < n_t) & (key >= tk[j]);
             } else {
-              bin += (key >= t_key[b]);
+              for (int b = 0; b < n_t; ++b) bin += (key >= t_key[b]);
+            }
+          } else {
+            for (int b = 0; b < n_t; ++b) {
+              if (t_eq[b] > 1) {   // uniform branch: ordered split of equal keys
+                const bool eq = valid && (key == t_key[b]);
+                const int c0 = carry_s[b];
+                int tot;
+                const int pos = block_excl_count(eq, sh_cnt, &tot) + c0;
+                bin += (key > t_key[b]) || (eq && pos >= t_rank[b]);
+                __syncthreads();
+                if (tid == 0) carry_s[b] = c0 + tot;
+                __syncthreads();
+              } else {
+                bin += (key >= t_key[b]);
+              }
             }
           }
+          if (valid) {
+            sc = span_of(sc, i);
+            atomicAdd(&hist[bin * ncell + cell_of(sc, i)], 1);
+          }
         }
-        if (valid) {
-          const int cell = scaled_index(r, M, rows, fr) * M + scaled_index(c, M, cols, fc);
-          atomicAdd(&hist[bin * ncell + cell], 1);
-        }
-        c += dr;
-        r += dq;
-        if (c >= cols) { c -= cols; ++r; }
       }
-    }
-    __syncthreads();
+      __syncthreads();
     }
     // ---- plug-in MI from the counts (fixed summation order)
     if (tid < K) {
       int sum = 0;
-      for (int cc = 0; cc < ncell; ++cc) sum += hist[tid * ncell + cc];
+      for (int cc = 0; cc < ncell; ++cc) sum += jh[tid * ncell + cc];
       nb_s[tid] = sum;
     }
     if (tid < ncell) {
       int sum = 0;
-      for (int b = 0; b < K; ++b) sum += hist[b * ncell + tid];
+      for (int b = 0; b < K; ++b) sum += jh[b * ncell + tid];
       nc_s[tid] = sum;
     }
     __syncthreads();
     double part = 0.0;
     for (int i = tid; i < K * ncell; i += kThreads) {
-      const int n = hist[i];
+      const int n = jh[i];
       if (n > 0) {
         const double nn = (double)n, NN = (double)N;
         part += (nn / NN) * log(nn * NN / ((double)nb_s[i / ncell] * (double)nc_s[i % ncell]));
@@ -671,7 +725,7 @@ __device__ void stats_body(const StatsArgs& a) {
 
 
 // One wave, one lane per group (G <= 64); wave reductions in a fixed order.
-__device__ void finalize_layer(const FinalArgs& a, int layer, int lane) {
+__device__ __forceinline__ void finalize_layer(const FinalArgs& a, int layer, int lane) {
   float* scal = a.scal + (size_t)layer * a.sc;
   char* blk = a.state + (size_t)layer * a.state_stride;
   StateHeader* hdr = reinterpret_cast<StateHeader*>(blk);

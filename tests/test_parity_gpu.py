@@ -360,6 +360,35 @@ def test_rising_and_spiking_logits(dtype, d, H, G, W):
              Vs=Vs)
 
 
+@pytest.mark.parametrize("kind", ["zero", "three"])
+def test_ties_beyond_the_key_cache(kind):
+    """30,000 visual tokens, more than the statistics kernel keeps in LDS, so
+    every rank-binning pass reads S from memory.  Keys all zero (every
+    interior score ties) or drawn from three one-hot vectors (three values,
+    each shared by about 10,000 tokens): the bin edges fall inside runs of equal
+    keys, split by token order.  The three-vector case pools over one token:
+    a wider pool mixes neighbours, and neighbourhoods that are permutations
+    of each other give equal sums that float32 and float64 round apart, so
+    the two sides would order those tokens differently."""
+    p = params_for(2, prior_active=True)
+    if kind == "three":
+        p.pool_kernel = 1
+    H, G, d, W, L = 8, 2, 128, 8, 30100
+    Qs, Ks, Vs = WL.random_case(5, 1, H, G, d, L, W, "bf16")
+    if kind == "zero":
+        Ks = np.zeros_like(Ks)
+    else:
+        # zero, 2 e_3 or -e_7: every logit is one exact product, so equal keys
+        # give bit-equal scores on both sides whatever the summation order
+        basis = np.zeros((3, d), np.float32)
+        basis[1, 3], basis[2, 7] = 2.0, -1.0
+        pick = np.random.default_rng([5, 3]).integers(0, 3, size=(1, G, L))
+        Ks = WL.f32_to_bf16_bits(basis[pick])
+    spans = [(10, 150, 200, 1)]
+    run_case(f"ties uncached {kind}", H, G, d, W, L, spans, 1, 3000, "bf16", p, Qs=Qs,
+             Ks=Ks, Vs=Vs, n_layers=1)
+
+
 def test_frame_size_change_resets_stability():
     """Two steps whose current frames differ in size: m_g restarts, phi = 0."""
     p = params_for(3, prior_active=True)
