@@ -66,6 +66,7 @@ struct StatsArgs {
 constexpr int kThreads = 1024;
 constexpr int kWaves = kThreads / 64;
 constexpr int kBatch = 8;                 // loads in flight per thread
+constexpr int kKeyBatch = 8;              // keys per thread per rank-binning step
 constexpr int kHistInts = 16384;          // 64 KiB: digit or joint histograms
 constexpr int kKeyCache = 20 * 1024;      // visual keys kept in LDS
 constexpr int kCand = 2048;               // keys in the edges' first-digit buckets
@@ -74,14 +75,22 @@ constexpr int kJointOff = 8192;           // joint histogram slot when digits fo
 constexpr size_t kStatsLds =
     (size_t)kHistInts * 4 + (size_t)kKeyCache * 4 + (size_t)kCand * 4;
 
-// floor(x * M / n) for 0 <= x < n, without an integer division: the float
-// estimate is within one of the quotient (x * M < 2^31, M <= 16).
+// floor(x * M / n) without an integer division, for 0 <= x < 2^22 and
+// x * M < 2^31: the float estimate is within one of the quotient, and one
+// correction step makes it exact.
 __device__ inline int scaled_index(int x, int M, int n, float m_over_n) {
   int q = (int)((float)x * m_over_n);
   const int xm = x * M;
   if (q * n > xm) --q;
   else if ((q + 1) * n <= xm) ++q;
   return q;
+}
+
+// Sum over the wave's lanes (integers: exact in any order).
+__device__ inline int wave_sum_i(int v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o);
+  return v;
 }
 
 __device__ __forceinline__ void stats_body(const StatsArgs& a) {
@@ -261,69 +270,97 @@ __device__ __forceinline__ void stats_body(const StatsArgs& a) {
   double mi = 0.0;
 
   if (N > 0) {
-    // span table to LDS (a uniform index keeps the argument in scalar loads)
-    if (tid == 0) {
-      for (int s = 0; s < a.sp.n; ++s) {
+    // span table to LDS, a span per wave (a wave-uniform index keeps the
+    // argument in scalar loads)
+    for (int s = __builtin_amdgcn_readfirstlane(wave); s < a.sp.n; s += kWaves) {
+      if (lane == 0) {
         sp_off[s] = a.sp.off[s];
         sp_start[s] = a.sp.start[s];
         sp_rows[s] = a.sp.rows[s];
         sp_cols[s] = a.sp.cols[s];
       }
-      sp_off[a.sp.n] = N;
     }
+    if (tid == 0) sp_off[a.sp.n] = N;
     __syncthreads();
     // Visual index i (ascending per thread) -> its span, by a cursor s.
     auto span_of = [&](int s, int i) {
       while (sp_off[s + 1] <= i) ++s;
       return s;
     };
-    // The kBatch keys i0 + u * kThreads of this thread (0 past N), read from
-    // S with kBatch loads in flight.  Returns the advanced cursor.
-    auto fetch = [&](int i0, int s, uint32_t (&kv)[kBatch]) {
-      float v[kBatch];
+    // Token positions of a thread's visual indices (ascending): the span
+    // cursor keeps the current span's end and its token - index offset.
+    int f_s = 0, f_end = 0, f_base = 0;
+    auto token_of = [&](int i) {
+      if (i >= f_end) {
+        f_s = span_of(f_s, i);
+        f_end = sp_off[f_s + 1];
+        f_base = sp_start[f_s] - sp_off[f_s];
+      }
+      return f_base + i;
+    };
+    auto fetch_reset = [&]() { f_s = 0; f_end = 0; };
+    // The kKeyBatch keys i0 + u * kThreads of this thread (0 past N), read
+    // from S with kKeyBatch loads in flight.
+    auto fetch = [&](int i0, uint32_t (&kv)[kKeyBatch]) {
+      float v[kKeyBatch];
 #pragma unroll
-      for (int u = 0; u < kBatch; ++u) {
+      for (int u = 0; u < kKeyBatch; ++u) {
         const int i = i0 + u * kThreads;
-        v[u] = 0.f;
-        if (i < N) {
-          s = span_of(s, i);
-          v[u] = Sg[sp_start[s] + (i - sp_off[s])];
-        }
+        v[u] = i < N ? Sg[token_of(i)] : 0.f;
       }
 #pragma unroll
-      for (int u = 0; u < kBatch; ++u) kv[u] = i0 + u * kThreads < N ? fkey(v[u]) : 0u;
-      return s;
+      for (int u = 0; u < kKeyBatch; ++u) kv[u] = i0 + u * kThreads < N ? fkey(v[u]) : 0u;
     };
     // the same from the key cache, or from S when the keys are not cached
-    auto keys = [&](int i0, int s, uint32_t (&kv)[kBatch]) {
-      if (!cached) return fetch(i0, s, kv);
+    auto keys = [&](int i0, uint32_t (&kv)[kKeyBatch]) {
+      if (!cached) {
+        fetch(i0, kv);
+        return;
+      }
 #pragma unroll
-      for (int u = 0; u < kBatch; ++u) {
+      for (int u = 0; u < kKeyBatch; ++u) {
         const int i = i0 + u * kThreads;
         kv[u] = i < N ? kc[i] : 0u;
       }
-      return s;
     };
-    // grid cell of visual index i in span s
-    auto cell_of = [&](int s, int i) {
-      const int p = i - sp_off[s], cols = sp_cols[s], rows = sp_rows[s];
-      int r = (int)((float)p * (1.0f / (float)cols));
-      if (r * cols > p) --r;
-      else if ((r + 1) * cols <= p) ++r;
-      const int c = p - r * cols;
-      return scaled_index(r, M, rows, (float)M / (float)rows) * M +
-             scaled_index(c, M, cols, (float)M / (float)cols);
+    // Grid cell of visual index i.  A pass visits a thread's indices in
+    // steps of kThreads, so (row, col) step inside a span and are recomputed
+    // by a division only when the index enters another span.
+    int q_s = 0, q_r = 0, q_c = 0, q_end = 0, q_next = -1, q_rows = 1, q_cols = 1,
+        q_dq = 0, q_dr = 0;
+    float q_fr = 0.f, q_fc = 0.f;
+    auto cell_at = [&](int i) {
+      if (i != q_next || i >= q_end) {
+        q_s = span_of(q_s, i);
+        q_rows = sp_rows[q_s];
+        q_cols = sp_cols[q_s];
+        q_end = sp_off[q_s + 1];
+        const int p = i - sp_off[q_s];
+        q_r = scaled_index(p, 1, q_cols, 1.0f / (float)q_cols);   // p / cols
+        q_c = p - q_r * q_cols;
+        q_dq = kThreads / q_cols;
+        q_dr = kThreads - q_dq * q_cols;
+        q_fr = (float)M / (float)q_rows;
+        q_fc = (float)M / (float)q_cols;
+      } else {
+        q_c += q_dr;
+        q_r += q_dq;
+        if (q_c >= q_cols) { q_c -= q_cols; ++q_r; }
+      }
+      q_next = i + kThreads;
+      return scaled_index(q_r, M, q_rows, q_fr) * M + scaled_index(q_c, M, q_cols, q_fc);
     };
+    auto cell_reset = [&]() { q_s = 0; q_next = -1; };
 
     // ---- visual keys (LDS when they fit), min and max
     uint32_t lo = 0xFFFFFFFFu, hi = 0u;
     {
-      int s = 0;
-      for (int i0 = tid; i0 < N; i0 += kBatch * kThreads) {
-        uint32_t kv[kBatch];
-        s = fetch(i0, s, kv);
+      fetch_reset();
+      for (int i0 = tid; i0 < N; i0 += kKeyBatch * kThreads) {
+        uint32_t kv[kKeyBatch];
+        fetch(i0, kv);
 #pragma unroll
-        for (int u = 0; u < kBatch; ++u) {
+        for (int u = 0; u < kKeyBatch; ++u) {
           const int i = i0 + u * kThreads;
           if (i < N) {
             if (cached) kc[i] = kv[u];
@@ -455,25 +492,25 @@ __device__ __forceinline__ void stats_body(const StatsArgs& a) {
         while (u < nu && u_hi[u] != h) ++u;
         if (u < nu) atomicAdd(&hist[u * nb + ((key >> shift) & (nb - 1))], 1);
       };
-      if (first && cached) {
-        // every key shares the prefix: one histogram, eight keys in flight
-        for (int i0 = tid; i0 < N; i0 += 8 * kThreads) {
-          uint32_t kv[8];
+      if (first) {
+        // every key shares the prefix: one histogram
+        fetch_reset();
+        for (int i0 = tid; i0 < N; i0 += kKeyBatch * kThreads) {
+          uint32_t kv[kKeyBatch];
+          keys(i0, kv);
 #pragma unroll
-          for (int u = 0; u < 8; ++u) kv[u] = kc[min(i0 + u * kThreads, N - 1)];
-#pragma unroll
-          for (int u = 0; u < 8; ++u)
+          for (int u = 0; u < kKeyBatch; ++u)
             if (i0 + u * kThreads < N) atomicAdd(&hist[(kv[u] >> shift) & (nb - 1)], 1);
         }
       } else if (compact) {
         for (int i = tid; i < n_c; i += kThreads) count(ck[i]);
       } else {
-        int s = 0;
-        for (int i0 = tid; i0 < N; i0 += kBatch * kThreads) {
-          uint32_t kv[kBatch];
-          s = keys(i0, s, kv);
+        fetch_reset();
+        for (int i0 = tid; i0 < N; i0 += kKeyBatch * kThreads) {
+          uint32_t kv[kKeyBatch];
+          keys(i0, kv);
 #pragma unroll
-          for (int u = 0; u < kBatch; ++u)
+          for (int u = 0; u < kKeyBatch; ++u)
             if (i0 + u * kThreads < N) count(kv[u]);
         }
       }
@@ -545,27 +582,31 @@ __device__ __forceinline__ void stats_body(const StatsArgs& a) {
           for (int j = 0; j < 8; ++j)
             eb[j] = j < n_t ? ((t_key[j] >> shift) & (uint32_t)(nb - 1)) : 0xFFFFFFFFu;
           __syncthreads();
-          int s = 0, sc = 0;
-          for (int i0 = tid; i0 < N; i0 += kBatch * kThreads) {
-            uint32_t kv[kBatch];
-            s = keys(i0, s, kv);
+          fetch_reset();
+          auto fuse_key = [&](int i, uint32_t key) {
+            const uint32_t d = (key >> shift) & (uint32_t)(nb - 1);
+            const int cell = cell_at(i);
+            if ((bucket_bits[d >> 5] >> (d & 31)) & 1u) {
+              const int sg = seg_of_bucket(d);
+              const int pos = seg_off[sg] + atomicAdd(&seg_cur[sg], 1);
+              ck[pos] = key;
+              cv[pos] = ((uint32_t)cell << 24) | (uint32_t)i;
+            } else {
+              atomicAdd(&jh[lower_edges(d) * ncell + cell], 1);
+            }
+          };
+          cell_reset();
+          if (cached) {   // keys in LDS: one copy of the body
+#pragma unroll 2
+            for (int i = tid; i < N; i += kThreads) fuse_key(i, kc[i]);
+          } else {        // kKeyBatch loads in flight
+            fetch_reset();
+            for (int i0 = tid; i0 < N; i0 += kKeyBatch * kThreads) {
+              uint32_t kv[kKeyBatch];
+              fetch(i0, kv);
 #pragma unroll
-            for (int u = 0; u < kBatch; ++u) {
-              const int i = i0 + u * kThreads;
-              if (i < N) {
-                const uint32_t key = kv[u];
-                const uint32_t d = (key >> shift) & (uint32_t)(nb - 1);
-                sc = span_of(sc, i);
-                const int cell = cell_of(sc, i);
-                if ((bucket_bits[d >> 5] >> (d & 31)) & 1u) {
-                  const int sg = seg_of_bucket(d);
-                  const int pos = seg_off[sg] + atomicAdd(&seg_cur[sg], 1);
-                  ck[pos] = key;
-                  cv[pos] = ((uint32_t)cell << 24) | (uint32_t)i;
-                } else {
-                  atomicAdd(&jh[lower_edges(d) * ncell + cell], 1);
-                }
-              }
+              for (int u = 0; u < kKeyBatch; ++u)
+                if (i0 + u * kThreads < N) fuse_key(i0 + u * kThreads, kv[u]);
             }
           }
           __syncthreads();
@@ -578,12 +619,12 @@ __device__ __forceinline__ void stats_body(const StatsArgs& a) {
         } else if (done + width < 32 && cand_total <= ccap) {
           // compaction: each bucket's keys in its own segment (in any order
           // inside it)
-          int s = 0;
-          for (int i0 = tid; i0 < N; i0 += kBatch * kThreads) {
-            uint32_t kv[kBatch];
-            s = keys(i0, s, kv);
+          fetch_reset();
+          for (int i0 = tid; i0 < N; i0 += kKeyBatch * kThreads) {
+            uint32_t kv[kKeyBatch];
+            keys(i0, kv);
 #pragma unroll
-            for (int u = 0; u < kBatch; ++u) {
+            for (int u = 0; u < kKeyBatch; ++u) {
               const uint32_t dg = (kv[u] >> shift) & (uint32_t)(nb - 1);
               if (i0 + u * kThreads < N && ((bucket_bits[dg >> 5] >> (dg & 31)) & 1u)) {
                 const int sg = seg_of_bucket(dg);
@@ -657,15 +698,14 @@ __device__ __forceinline__ void stats_body(const StatsArgs& a) {
 #pragma unroll
       for (int j = 0; j < 8; ++j) tk[j] = j < n_t ? t_key[j] : 0u;
       __syncthreads();
-      int s = 0, sc = 0;
-      for (int i0 = 0; i0 < N; i0 += kBatch * kThreads) {
-        uint32_t kv[kBatch];
-        s = keys(i0 + tid, s, kv);
-#pragma unroll
-        for (int u = 0; u < kBatch; ++u) {
-          const int i = i0 + u * kThreads + tid;
+      fetch_reset();
+      cell_reset();
+#pragma unroll 1
+      for (int i0 = 0; i0 < N; i0 += kThreads) {
+        {
+          const int i = i0 + tid;
           const bool valid = i < N;
-          const uint32_t key = kv[u];
+          const uint32_t key = valid ? (cached ? kc[i] : fkey(Sg[token_of(i)])) : 0u;
           int bin = 0;
           if (!any_tie) {
             if (n_t <= 8) {
@@ -690,19 +730,17 @@ __device__ __forceinline__ void stats_body(const StatsArgs& a) {
               }
             }
           }
-          if (valid) {
-            sc = span_of(sc, i);
-            atomicAdd(&hist[bin * ncell + cell_of(sc, i)], 1);
-          }
+          if (valid) atomicAdd(&hist[bin * ncell + cell_at(i)], 1);
         }
       }
       __syncthreads();
     }
-    // ---- plug-in MI from the counts (fixed summation order)
-    if (tid < K) {
+    // ---- plug-in MI from the counts (fixed summation order; integer sums)
+    for (int b = wave; b < K; b += kWaves) {   // bin totals: a wave per bin
       int sum = 0;
-      for (int cc = 0; cc < ncell; ++cc) sum += jh[tid * ncell + cc];
-      nb_s[tid] = sum;
+      for (int cc = lane; cc < ncell; cc += 64) sum += jh[b * ncell + cc];
+      sum = wave_sum_i(sum);
+      if (lane == 0) nb_s[b] = sum;
     }
     if (tid < ncell) {
       int sum = 0;
