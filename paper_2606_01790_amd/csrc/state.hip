@@ -17,14 +17,19 @@
 // ceil(b N / K), found together by one MSB-first radix select over
 // order-preserving 32-bit keys: the bits every key shares are skipped and
 // the first digit is 12 bits wide (one LDS histogram, block-wide scan).
-// When few keys (<= 256) share the edges' first-digit buckets, the joint
-// histogram pass itself bins every other key (its bin is the number of edges
-// in lower buckets) and collects the few, which are then ranked directly and
-// binned exactly.  Otherwise those keys are compacted into per-bucket
-// segments, later 8-bit digits (one histogram per distinct edge prefix, one
-// wave per edge) finish the edges, and the joint histogram pass bins every
-// key by comparison, splitting equal keys at an edge by token index with an
-// ordered block scan, so ties resolve exactly as the ranking defines.
+// The keys are cached in LDS up to 20K of them; beyond that every pass reads
+// S, walking the visual tokens as one index space with a span cursor.
+// Fused path (the edges' first-digit buckets hold at most 1024 keys, or
+// 10240 when the keys are not cached and the key cache holds candidates):
+// the joint histogram pass bins every key outside those buckets (its bin is
+// the number of edges in lower buckets) and keeps the others with their cell
+// and token index; up to 256 of them rank themselves directly, more are
+// finished by 8-bit digits (one histogram per distinct edge prefix, one wave
+// per edge); then each kept key is binned, equal keys at an edge split by
+// token index.  Otherwise the keys in those buckets are compacted for the
+// later digits, and the joint histogram pass bins every key by comparison,
+// splitting equal keys at an edge with an ordered block scan.  Either way
+// ties resolve exactly as the ranking defines.
 #include "device_common.h"
 #include "internal.h"
 
@@ -325,7 +330,8 @@ __device__ __forceinline__ void stats_body(const StatsArgs& a) {
     };
     // Grid cell of visual index i.  A pass visits a thread's indices in
     // steps of kThreads, so (row, col) step inside a span and are recomputed
-    // by a division only when the index enters another span.
+    // from the index (a float-estimated division) only when it enters
+    // another span.
     int q_s = 0, q_r = 0, q_c = 0, q_end = 0, q_next = -1, q_rows = 1, q_cols = 1,
         q_dq = 0, q_dr = 0;
     float q_fr = 0.f, q_fc = 0.f;
