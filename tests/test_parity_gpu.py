@@ -389,6 +389,48 @@ def test_ties_beyond_the_key_cache(kind):
              Ks=Ks, Vs=Vs, n_layers=1)
 
 
+@pytest.mark.parametrize("rows,cols", [(50, 60), (150, 200)])
+def test_pairwise_tied_keys(rows, cols):
+    """Every odd token repeats the key of the token before it, and the pool
+    covers one token, so scores tie in pairs and bin edges fall inside ties.
+    3,000 visual tokens keep their keys in LDS; 30,000 do not.  Both take the
+    fused binning pass, which splits a tie at an edge by token order among
+    the kept keys."""
+    p = params_for(2, prior_active=True)
+    p.pool_kernel = 1
+    H, G, d, W = 8, 2, 128, 8
+    L = rows * cols + 100
+    Qs, Ks, Vs = WL.random_case(9, 1, H, G, d, L, W, "bf16")
+    Ks = Ks.copy()
+    Ks[:, :, 1::2] = Ks[:, :, 0:-1:2][:, :, :Ks[:, :, 1::2].shape[2]]
+    spans = [(10, rows, cols, 1)]
+    run_case(f"pair ties {rows}x{cols}", H, G, d, W, L, spans, 1, rows * cols // 5, "bf16", p,
+             Qs=Qs, Ks=Ks, Vs=Vs, n_layers=1)
+
+
+@pytest.mark.parametrize("scale", [1, 10])
+def test_sixty_four_spans_of_odd_shapes(scale):
+    """The maximum of 64 visual spans (one frame each, three text tokens
+    between them), cycling through 1x1, one row of 150*scale, one column of
+    150*scale, 7x9, 13x17, 3x(10*scale), (4*scale)x(4*scale) and 2x3: rows
+    longer than the 1024-token step of a pass, one-column spans, and many
+    span changes per thread.  About 5,200 visual tokens at scale 1 (keys
+    kept in LDS) and 41,500 at scale 10 (keys read from memory)."""
+    p = params_for(3, prior_active=True)
+    shapes = [(1, 1), (1, 150 * scale), (150 * scale, 1), (7, 9), (13, 17), (3, 10 * scale),
+              (4 * scale, 4 * scale), (2, 3)]
+    spans, t = [], 5
+    for f in range(64):
+        r, c = shapes[f % len(shapes)]
+        spans.append((t, r, c, f + 1))
+        t += r * c + 3
+    H, G, d, W = 8, 2, 64, 8
+    L = t + 40 + W
+    n_vis = sum(r * c for _, r, c, _ in spans)
+    run_case(f"64 spans x{scale}", H, G, d, W, L, spans, 64, n_vis // 10, "bf16", p, seed=17,
+             n_layers=1)
+
+
 def test_frame_size_change_resets_stability():
     """Two steps whose current frames differ in size: m_g restarts, phi = 0."""
     p = params_for(3, prior_active=True)
