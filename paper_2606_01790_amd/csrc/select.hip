@@ -15,6 +15,8 @@
 //      its selected tokens (keys past the cut, plus the lowest-index ties at
 //      the cut) with ballots, and writes them at its segment's offset, so idx
 //      comes out ascending.
+// Keys past the LDS cache (28K tokens) are read back from s; those passes
+// keep eight loads in flight per thread.
 #include "device_common.h"
 #include "internal.h"
 
@@ -80,6 +82,20 @@ __global__ __launch_bounds__(kThreads) void select_kernel(SelArgs a) {
   const float inv_t = 1.0f / T;
   const float gl = (float)a.G * lam;
 
+  // Keys of tokens t0 + u * step, u < kBatch, at or past the LDS cache
+  // (0xFFFFFFFF past Lp), read back from s with kBatch loads in flight.
+  auto far_keys = [&](int t0, int step, uint32_t (&kv)[kBatch]) {
+    float v[kBatch];
+#pragma unroll
+    for (int u = 0; u < kBatch; ++u) {
+      const int t = t0 + u * step;
+      v[u] = t < a.Lp ? s_out[t] : 0.f;
+    }
+#pragma unroll
+    for (int u = 0; u < kBatch; ++u) kv[u] = t0 + u * step < a.Lp ? ~fkey(v[u]) : 0xFFFFFFFFu;
+  };
+  const int n_near = min(a.cache, a.Lp);   // tokens whose keys are in LDS
+
   // ---- 1. fused score; keys order tokens by descending s
   uint32_t lo = 0xFFFFFFFFu, hi = 0u;
   int cur = 0;   // first span that does not end at or before this thread's token
@@ -142,9 +158,13 @@ __global__ __launch_bounds__(kThreads) void select_kernel(SelArgs a) {
       for (int i = tid; i < nb; i += kThreads) hist[i] = 0;
       __syncthreads();
       // every key shares the prefix: one histogram of the first digit
-      for (int t = tid; t < a.Lp; t += kThreads) {
-        const uint32_t k = t < a.cache ? keys[t] : ~fkey(s_out[t]);
-        atomicAdd(&hist[(k >> shift) & (nb - 1)], 1);
+      for (int t = tid; t < n_near; t += kThreads) atomicAdd(&hist[(keys[t] >> shift) & (nb - 1)], 1);
+      for (int t0 = n_near + tid; t0 < a.Lp; t0 += kBatch * kThreads) {
+        uint32_t kv[kBatch];
+        far_keys(t0, kThreads, kv);
+#pragma unroll
+        for (int u = 0; u < kBatch; ++u)
+          if (t0 + u * kThreads < a.Lp) atomicAdd(&hist[(kv[u] >> shift) & (nb - 1)], 1);
       }
       __syncthreads();
       int c[4], sum = 0;
@@ -175,15 +195,23 @@ __global__ __launch_bounds__(kThreads) void select_kernel(SelArgs a) {
         // the keys of the cut's bucket, in any order
         const uint32_t pre = key_hi(ck, shift);
         const uint64_t below = lane == 0 ? 0ull : (~0ull >> (64 - lane));
-        for (int t0 = 0; t0 < a.Lp; t0 += kThreads) {
-          const int t = t0 + tid;
-          const uint32_t k = t < a.Lp ? (t < a.cache ? keys[t] : ~fkey(s_out[t])) : 0u;
-          const bool m = t < a.Lp && key_hi(k, shift) == pre;
+        auto keep = [&](uint32_t k, bool valid) {   // the whole wave calls it
+          const bool m = valid && key_hi(k, shift) == pre;
           const uint64_t bal = __ballot(m);
           int base = 0;
           if (lane == 0 && bal) base = atomicAdd(&n_cand, __popcll(bal));
           base = __shfl(base, 0);
           if (m) cand[base + __popcll(bal & below)] = k;
+        };
+        for (int t0 = 0; t0 < n_near; t0 += kThreads) {
+          const int t = t0 + tid;
+          keep(t < n_near ? keys[t] : 0u, t < n_near);
+        }
+        for (int b0 = n_near; b0 < a.Lp; b0 += kBatch * kThreads) {
+          uint32_t kv[kBatch];
+          far_keys(b0 + tid, kThreads, kv);
+#pragma unroll
+          for (int u = 0; u < kBatch; ++u) keep(kv[u], b0 + u * kThreads + tid < a.Lp);
         }
         __syncthreads();
         compact = true;
@@ -227,10 +255,17 @@ __global__ __launch_bounds__(kThreads) void select_kernel(SelArgs a) {
             atomicAdd(&hist[wave * 256 + ((k >> shift) & (nb - 1))], 1);
         }
       } else {
-        for (int t = tid; t < a.Lp; t += kThreads) {
-          const uint32_t k = t < a.cache ? keys[t] : ~fkey(s_out[t]);
+        auto count = [&](uint32_t k) {
           if (key_hi(k, shift + width) == want)
             atomicAdd(&hist[wave * 256 + ((k >> shift) & (nb - 1))], 1);
+        };
+        for (int t = tid; t < n_near; t += kThreads) count(keys[t]);
+        for (int t0 = n_near + tid; t0 < a.Lp; t0 += kBatch * kThreads) {
+          uint32_t kv[kBatch];
+          far_keys(t0, kThreads, kv);
+#pragma unroll
+          for (int u = 0; u < kBatch; ++u)
+            if (t0 + u * kThreads < a.Lp) count(kv[u]);
         }
       }
       __syncthreads();
@@ -262,13 +297,22 @@ __global__ __launch_bounds__(kThreads) void select_kernel(SelArgs a) {
   const int seg = ((a.Lp + kWaves * 64 - 1) / (kWaves * 64)) * 64;
   const int t0 = wave * seg, t1 = min(t0 + seg, a.Lp);
   const uint64_t below = lane == 0 ? 0ull : (~0ull >> (64 - lane));
+  // the segment's tokens in LDS, then the ones past the cache
+  const int tn = min(max(t0, n_near), t1);
   int n_strict = 0, n_eq = 0;
-  for (int base = t0; base < t1; base += 64) {
-    const int t = base + lane;
-    uint32_t k = 0xFFFFFFFFu;
-    if (t < t1) k = t < a.cache ? keys[t] : ~fkey(s_out[t]);
+  auto tally = [&](int t, uint32_t k) {
     n_strict += __popcll(__ballot(t < t1 && k < ck));
     n_eq += __popcll(__ballot(t < t1 && k == ck));
+  };
+  for (int base = t0; base < tn; base += 64) {
+    const int t = base + lane;
+    tally(t < tn ? t : t1, t < tn ? keys[t] : 0xFFFFFFFFu);
+  }
+  for (int b = tn; b < t1; b += kBatch * 64) {
+    uint32_t kv[kBatch];
+    far_keys(b + lane, 64, kv);
+#pragma unroll
+    for (int u = 0; u < kBatch; ++u) tally(b + u * 64 + lane, kv[u]);
   }
   if (lane == 0) { wsel[wave] = n_strict; weq[wave] = n_eq; }
   __syncthreads();
@@ -278,10 +322,7 @@ __global__ __launch_bounds__(kThreads) void select_kernel(SelArgs a) {
     eq_off += weq[w];
   }
   int32_t* out = a.idx + (size_t)layer * a.B;
-  for (int base = t0; base < t1; base += 64) {
-    const int t = base + lane;
-    uint32_t k = 0xFFFFFFFFu;
-    if (t < t1) k = t < a.cache ? keys[t] : ~fkey(s_out[t]);
+  auto emit = [&](int t, uint32_t k) {   // tokens in ascending order
     const bool strict = t < t1 && k < ck;
     const bool eq = t < t1 && k == ck;
     const uint64_t meq = __ballot(eq);
@@ -292,6 +333,16 @@ __global__ __launch_bounds__(kThreads) void select_kernel(SelArgs a) {
     if (sel && pos < a.B) out[pos] = t;
     off += __popcll(msel);
     eq_off += __popcll(meq);
+  };
+  for (int base = t0; base < tn; base += 64) {
+    const int t = base + lane;
+    emit(t < tn ? t : t1, t < tn ? keys[t] : 0xFFFFFFFFu);
+  }
+  for (int b = tn; b < t1; b += kBatch * 64) {
+    uint32_t kv[kBatch];
+    far_keys(b + lane, 64, kv);
+#pragma unroll
+    for (int u = 0; u < kBatch; ++u) emit(b + u * 64 + lane, kv[u]);
   }
 }
 
