@@ -431,6 +431,27 @@ def test_sixty_four_spans_of_odd_shapes(scale):
              n_layers=1)
 
 
+@pytest.mark.parametrize("n_bins,grid", [(1, 8), (2, 1), (8, 16), (16, 8), (33, 4), (64, 16)])
+@pytest.mark.parametrize("rows,cols", [(40, 60), (150, 160)])
+def test_rank_bins_and_grid_extremes(n_bins, grid, rows, cols):
+    """Rank-bin counts K from 1 (no edges) to 64 and grids M from 1 to 16,
+    with 2,400 visual tokens (keys in LDS) and 24,000 (keys read from
+    memory): K = 33 is the largest that takes the fused pass, K = 64 with
+    M = 16 fills the whole joint histogram.  MI and w are compared stage-wise
+    and end to end; lambda = 0 keeps beta = 1, because on random inputs the
+    groups' MIs can lie within rounding of each other (1.5e-4 apart at
+    K = 33 on 24,000 tokens), where the min-max prior may rank them either
+    way and the fused score then differs by the prior's full weight."""
+    p = params_for(2, prior_active=True)
+    p.n_bins, p.grid = n_bins, grid
+    p.lam = 0.0
+    H, G, d, W = 8, 2, 64, 8
+    L = rows * cols + 200
+    spans = [(100, rows, cols, 1)]
+    run_case(f"K={n_bins} M={grid} {rows}x{cols}", H, G, d, W, L, spans, 1, rows * cols // 4,
+             "bf16", p, seed=n_bins * 31 + grid, n_layers=1)
+
+
 def test_frame_size_change_resets_stability():
     """Two steps whose current frames differ in size: m_g restarts, phi = 0."""
     p = params_for(3, prior_active=True)
