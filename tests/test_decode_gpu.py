@@ -117,6 +117,36 @@ def test_decode_zero_query_is_the_value_mean():
         assert np.max(np.abs(got[0, h] - mean[h * G // H])) <= 1e-5
 
 
+def test_decode_reuses_one_workspace():
+    """Calls in a row on one workspace, left as the previous call wrote it,
+    with token counts that change the number of splits (1, 11, 3 and 20
+    splits, so each call's partials cover a different range)."""
+    H, G, d, nl = 28, 4, 128, 2
+    n_max = 5000
+    dev = torch.device("cuda:0")
+    q = random_bits(31, (nl, H, d))
+    k = random_bits(32, (nl, G, n_max, d))
+    v = random_bits(33, (nl, G, n_max, d))
+    dims = sk.make_dims(nl, H, G, d, n_max + 1, 1, sk.BF16)
+    ws = torch.zeros(sk.decode_workspace_bytes(dims, n_max), dtype=torch.uint8, device=dev)
+    qd = torch.from_numpy(q.view(np.int16)).to(dev)
+    kd = torch.from_numpy(k.view(np.int16)).to(dev)
+    vd = torch.from_numpy(v.view(np.int16)).to(dev)
+    lay = sk.KVLayout(G * n_max * d, n_max * d, d)
+    for n in (200, 2723, 700, n_max):
+        out = torch.zeros(nl * H * d, dtype=torch.float32, device=dev)
+        sk.decode(dims, qd, kd, vd, lay, n, out, ws)
+        torch.cuda.synchronize()
+        got = out.cpu().numpy().reshape(nl, H, d)
+        for layer in range(nl):
+            qf = WL.to_float64(q[layer], "bf16")
+            Kf = WL.to_float64(k[layer][:, :n], "bf16")
+            Vf = WL.to_float64(v[layer][:, :n], "bf16")
+            err = np.abs(got[layer] - O.decode_attention(qf, Kf, Vf))
+            assert np.all(err <= bound(qf, Kf, Vf)), f"n={n} L{layer}: max err {err.max()}"
+        say(f"reused workspace: n={n} ok")
+
+
 def test_decode_on_compressed_cache_of_the_stage():
     """The stage's own K'/V' (one 1920x1080 frame, Qwen2.5-VL-7B shape, top
     20%): decode over the B + W kept rows against the oracle on the same
