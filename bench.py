@@ -12,7 +12,9 @@ Prints one JSON line:
   value      compressed visual tokens per second per layer: the sum over
              trajectory steps and layers of N_vis, divided by the time;
   roofline   the dominant call's achieved algorithmic bandwidth against the
-             8 TB/s HBM peak, from HIP events on its stream;
+             8 TB/s HBM peak, or its algorithmic flops against the dense
+             MFMA peak when its intensity is above the ridge (the W = 64
+             trajectory), from HIP events on its stream;
   cpu_baseline  the fp64 CPU oracle on a bounded sample of the same work.
 """
 
@@ -29,6 +31,8 @@ if ROOT not in sys.path:
     sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBS = 8000.0
+# dense MFMA peaks by input type (TFLOP/s)
+MFMA_PEAK_TFLOPS = {"bf16": 2500.0, "f32": 157.3}
 METRIC = "compressed visual KV tokens/s per layer (score+select+gather); % HBM peak"
 
 
@@ -191,6 +195,7 @@ def per_call_timing(wl, spec, sk, torch, reps):
     """Average GPU time of each call, per trajectory step: `reps` launches of
     the call back to back, captured in a HIP graph and timed with HIP events
     on the replay stream.  update_state runs on a scratch state."""
+    from paper_2606_01790_amd import workload as WL
     p = wl.params
     scratch = wl.states[-2]
     per = {}
@@ -221,10 +226,13 @@ def per_call_timing(wl, spec, sk, torch, reps):
             g.replay()
             e1.record(stream)
             torch.cuda.synchronize()
-            d = per.setdefault(name, {"time": 0.0, "launches": 0, "bytes": 0})
+            d = per.setdefault(name, {"time": 0.0, "launches": 0, "bytes": 0, "flops": 0})
             d["time"] += e0.elapsed_time(e1) * 1e-3
             d["launches"] += reps
             d["bytes"] += reps * call_bytes(spec, s, name, wl.per_head)
+            if name == "score":   # the window-query/key contraction, counted once
+                d["flops"] += reps * spec.n_layers * WL.qk_flops(spec.H, spec.W, spec.L_p(s),
+                                                                 spec.d)
     return per
 
 
@@ -307,13 +315,22 @@ def main():
         dd = per[dom]
         avg_s = dd["time"] / dd["launches"]
         avg_b = dd["bytes"] / dd["launches"]
-        achieved = avg_b / avg_s / 1e9
-        roofline = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS,
-                    "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
-                    "traffic": measured_traffic(f"starkv_{dom}", workload),
-                    "kernel": f"starkv_{dom}",
-                    "avg_launch_us": round(avg_s * 1e6, 2),
-                    "alg_bytes_per_launch": int(avg_b)}
+        avg_f = dd["flops"] / dd["launches"]
+        mfma_peak = MFMA_PEAK_TFLOPS[spec.dtype]
+        # the bound is the roof the call's algorithmic intensity meets first
+        if avg_f / avg_b > mfma_peak * 1e12 / (HBM_PEAK_GBS * 1e9):
+            achieved = avg_f / avg_s / 1e12
+            roofline = {"bound": "mfma", "achieved": round(achieved, 1), "peak": mfma_peak,
+                        "unit": "TFLOP/s", "frac": round(achieved / mfma_peak, 4)}
+        else:
+            achieved = avg_b / avg_s / 1e9
+            roofline = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS,
+                        "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4)}
+        roofline.update({"traffic": measured_traffic(f"starkv_{dom}", workload),
+                         "kernel": f"starkv_{dom}",
+                         "avg_launch_us": round(avg_s * 1e6, 2),
+                         "alg_bytes_per_launch": int(avg_b),
+                         "alg_flops_per_launch": int(avg_f)})
         per_call_us = {n: round(per[n]["time"] / per[n]["launches"] * 1e6, 2) for n in per}
 
     cpu = None
