@@ -191,6 +191,20 @@ def call_bytes(spec, s, name, per_head=False):
     return nl * per
 
 
+def roofline_of(seconds, alg_bytes, alg_flops, dtype):
+    """Roofline of one launch: the roof its algorithmic intensity meets first,
+    HBM (GB/s against 8 TB/s) or the dense MFMA peak of its input type
+    (TFLOP/s), with the achieved rate and its fraction of that peak."""
+    mfma_peak = MFMA_PEAK_TFLOPS[dtype]
+    if alg_bytes > 0 and alg_flops / alg_bytes > mfma_peak * 1e12 / (HBM_PEAK_GBS * 1e9):
+        achieved = alg_flops / seconds / 1e12
+        return {"bound": "mfma", "achieved": round(achieved, 1), "peak": mfma_peak,
+                "unit": "TFLOP/s", "frac": round(achieved / mfma_peak, 4)}
+    achieved = alg_bytes / seconds / 1e9
+    return {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS,
+            "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4)}
+
+
 def per_call_timing(wl, spec, sk, torch, reps):
     """Average GPU time of each call, per trajectory step: `reps` launches of
     the call back to back, captured in a HIP graph and timed with HIP events
@@ -316,16 +330,7 @@ def main():
         avg_s = dd["time"] / dd["launches"]
         avg_b = dd["bytes"] / dd["launches"]
         avg_f = dd["flops"] / dd["launches"]
-        mfma_peak = MFMA_PEAK_TFLOPS[spec.dtype]
-        # the bound is the roof the call's algorithmic intensity meets first
-        if avg_f / avg_b > mfma_peak * 1e12 / (HBM_PEAK_GBS * 1e9):
-            achieved = avg_f / avg_s / 1e12
-            roofline = {"bound": "mfma", "achieved": round(achieved, 1), "peak": mfma_peak,
-                        "unit": "TFLOP/s", "frac": round(achieved / mfma_peak, 4)}
-        else:
-            achieved = avg_b / avg_s / 1e9
-            roofline = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS,
-                        "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4)}
+        roofline = roofline_of(avg_s, avg_b, avg_f, spec.dtype)
         roofline.update({"traffic": measured_traffic(f"starkv_{dom}", workload),
                          "kernel": f"starkv_{dom}",
                          "avg_launch_us": round(avg_s * 1e6, 2),

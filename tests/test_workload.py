@@ -129,3 +129,24 @@ def test_frames_keep_their_bytes_when_they_move():
     t3 = WL.Trajectory(WL.SPECS[3])
     k, _ = t3.layer_cache(1, 4)
     np.testing.assert_array_equal(k[:, 2 * 2691:3 * 2691], t3.frame_kv(1, 3)[0])
+
+
+def test_bench_roofline_bound_follows_intensity():
+    """The scoring call is HBM-bound at W = 32 (224 flop per K byte, below
+    the bf16 ridge of 312.5) and MFMA-bound at W = 64 (448); fp32 inputs take
+    the fp32 peak, whose ridge is 19.7."""
+    import bench
+    cases = [(3, "hbm"), (5, "mfma"), (1, "hbm")]
+    for cid, bound in cases:
+        spec = WL.SPECS[cid]
+        s = spec.steps
+        b = bench.call_bytes(spec, s, "score")
+        f = spec.n_layers * WL.qk_flops(spec.H, spec.W, spec.L_p(s), spec.d)
+        r = bench.roofline_of(1e-3, b, f, spec.dtype)
+        assert r["bound"] == bound, (cid, r)
+        if bound == "mfma":
+            assert r["peak"] == 2500.0 and r["unit"] == "TFLOP/s"
+            assert abs(r["achieved"] - f / 1e-3 / 1e12) < 0.1
+        else:
+            assert r["unit"] == "GB/s" and abs(r["achieved"] - b / 1e-3 / 1e9) < 0.1
+    assert bench.roofline_of(1.0, 1, 10 ** 6, "f32")["peak"] == 157.3
