@@ -253,7 +253,7 @@ def per_call_timing(wl, spec, sk, torch, reps):
 def main():
     args = parse()
     if args.gpus != 1:
-        print("bench.py: this build runs the compression stage on one GPU only; "
+        print("bench.py: the compression stage runs on one GPU only; "
               "a multi-GPU run is not supported (use --gpus 1).", file=sys.stderr)
         sys.exit(2)
     if args.decode:
