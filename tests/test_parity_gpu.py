@@ -573,6 +573,46 @@ def test_largest_window_row_block_f32():
     run_case("R=128 f32", 8, 2, 64, 32, 400, spans, 1, 60, "f32", p, seed=62, n_layers=1)
 
 
+def _bf16_unit_bits(rng, shape):
+    """bf16 bit patterns of magnitude in [1, 2) with random sign: random
+    64-bit words, each read as four bf16 values whose exponent bits are then
+    fixed at 127 (sign and seven mantissa bits stay random)."""
+    n = int(np.prod(shape))
+    assert n % 4 == 0
+    u = rng.integers(0, np.iinfo(np.uint64).max, n // 4, dtype=np.uint64, endpoint=True)
+    u &= np.uint64(0x807F807F807F807F)
+    u |= np.uint64(0x3F803F803F803F80)
+    return u.view(np.uint16).reshape(shape)
+
+
+def test_maximum_size_sixteen_million_visual_tokens():
+    """One 4000 x 4000 frame (N = 16e6 visual tokens, just under the 2^24
+    limit of the fused rank/joint-histogram path) in a cache of two KV groups
+    at d = 128: group 1's rows run from 2.05e9 to 4.1e9 elements into the K
+    cache, past 2^31 elements and 2^32 bytes (64-bit offsets in scoring and
+    in the gather), the rank pass runs uncached at its
+    largest and the selection streams 16e6 far keys.  Group 0's keys in the
+    lower half of the frame have half the magnitude, so its scores carry
+    spatial structure and its MI stands far above group 1's estimator bias
+    (the min-max prior is then well conditioned end to end)."""
+    p = params_for(3, prior_active=True)
+    rows = cols = 4000
+    N = rows * cols
+    H, G, d, W = 4, 2, 128, 8
+    L = 500 + N + 500 + W
+    B = N // 100
+    r = np.random.default_rng([64, 1])
+    Qs = WL.f32_to_bf16_bits(r.standard_normal((1, H, W, d), dtype=np.float32) *
+                             np.float32(0.3))
+    Ks = _bf16_unit_bits(r, (1, G, L, d))
+    Vs = _bf16_unit_bits(r, (1, G, L, d))
+    Ks[0, 0, 500 + N // 2:500 + N] &= np.uint16(0xFF7F)   # exponent 127 -> 126
+    assert G * L * d > 2 ** 31 and G * L * d * 2 > 2 ** 32
+    say(f"max size: inputs generated, K {Ks.nbytes / 2 ** 30:.1f} GiB")
+    run_case("max size", H, G, d, W, L, [(500, rows, cols, 1)], 1, B, "bf16", p,
+             n_layers=1, Qs=Qs, Ks=Ks, Vs=Vs)
+
+
 def test_no_visual_spans():
     """A text-only cache: no visual token, so MI = 0 and phi = 0 in every
     group, D = 1, and the selection runs on s-bar alone."""
