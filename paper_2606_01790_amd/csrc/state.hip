@@ -27,9 +27,12 @@
 // finished by 8-bit digits (one histogram per distinct edge prefix, one wave
 // per edge); then each kept key is binned, equal keys at an edge split by
 // token index.  Otherwise the keys in those buckets are compacted for the
-// later digits, and the joint histogram pass bins every key by comparison,
-// splitting equal keys at an edge with an ordered block scan.  Either way
-// ties resolve exactly as the ranking defines.
+// later digits, and the joint histogram pass bins every key by comparison.
+// Equal keys at an edge split by token index: with cached keys through an
+// ordered block scan of all keys; with uncached keys at a split point found
+// from per-chunk counts of the equal keys and an ordered scan of one chunk,
+// so that the binning pass itself reads in any order with loads in flight.
+// Either way ties resolve exactly as the ranking defines.
 #include "device_common.h"
 #include "internal.h"
 
@@ -77,6 +80,8 @@ constexpr int kKeyCache = 20 * 1024;      // visual keys kept in LDS
 constexpr int kCand = 2048;               // keys in the edges' first-digit buckets
 constexpr int kDirect = 256;              // candidates ranked directly, no more digits
 constexpr int kJointOff = 8192;           // joint histogram slot when digits follow
+constexpr int kTieChunks = 256;           // visual-index chunks for locating tie splits
+static_assert(63 * kTieChunks <= kKeyCache, "tie-split counts live in the key cache");
 constexpr size_t kStatsLds =
     (size_t)kHistInts * 4 + (size_t)kKeyCache * 4 + (size_t)kCand * 4;
 
@@ -692,10 +697,112 @@ __device__ __forceinline__ void stats_body(const StatsArgs& a) {
         atomicAdd(&jh[bin * ncell + cell], 1);
       }
       __syncthreads();
+    } else if (!cached) {
+      // ---- joint histogram of (bin, cell), keys read from S with kKeyBatch
+      // loads in flight, in any order.  Equal keys at a tied edge split by
+      // visual index (the ranking's tie rule): the split point t_vis comes
+      // from per-chunk counts of the equal keys (any order) and an ordered
+      // scan of the one chunk that holds the split.
+      for (int i = tid; i < K * ncell; i += kThreads) hist[i] = 0;
+      bool any_tie = false;
+      for (int b = 0; b < n_t; ++b) any_tie |= (t_eq[b] > 1);
+      // LDS arrays free in this branch (static LDS is at its limit):
+      // t_vis[b], the first visual index above tied edge b, in the cached
+      // branch's carries; the chunk and residual rank of a split in the
+      // first digit's results
+      int* const t_vis = carry_s;
+      int& tie_c = n_rank[0];
+      int& tie_r = n_rank[1];
+      if (any_tie) {
+        const int chunk =
+            ((N + kTieChunks - 1) / kTieChunks + kThreads - 1) / kThreads * kThreads;
+        int* tc = reinterpret_cast<int*>(kc);   // the key cache holds no keys here
+        for (int i = tid; i < n_t * kTieChunks; i += kThreads) tc[i] = 0;
+        __syncthreads();
+        fetch_reset();
+        for (int i0 = tid; i0 < N; i0 += kKeyBatch * kThreads) {
+          uint32_t kv[kKeyBatch];
+          fetch(i0, kv);
+#pragma unroll
+          for (int u = 0; u < kKeyBatch; ++u) {
+            const int i = i0 + u * kThreads;
+            if (i < N)
+              for (int b = 0; b < n_t; ++b)
+                if (t_eq[b] > 1 && kv[u] == t_key[b]) atomicAdd(&tc[b * kTieChunks + i / chunk], 1);
+          }
+        }
+        __syncthreads();
+        for (int b = 0; b < n_t; ++b) {
+          if (t_eq[b] <= 1) continue;   // uniform
+          if (wave == 0) {
+            // the chunk holding the equal key at position t_rank[b]
+            int c4[4], sum = 0;
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+              c4[j] = tc[b * kTieChunks + 4 * lane + j];
+              sum += c4[j];
+            }
+            const int inc = wave_incl_scan(sum);
+            const int total = __shfl(inc, 63);
+            const int r = t_rank[b];
+            if (lane == 0) t_vis[b] = N;
+            if (r >= total) {
+              if (lane == 0) tie_c = -1;
+            } else if (inc - sum <= r && r < inc) {
+              int run = inc - sum;
+              for (int j = 0; j < 4; ++j) {
+                if (r < run + c4[j]) {
+                  tie_c = 4 * lane + j;
+                  tie_r = r - run;
+                  break;
+                }
+                run += c4[j];
+              }
+            }
+          }
+          __syncthreads();
+          const int c = tie_c, rr = tie_r;
+          if (c >= 0) {
+            fetch_reset();
+            const int i_end = min(N, (c + 1) * chunk);
+            int carry = 0;   // equal keys seen so far in the chunk (uniform)
+            for (int i0 = c * chunk; i0 < i_end && carry <= rr; i0 += kThreads) {
+              const int i = i0 + tid;
+              const bool eq = i < i_end && fkey(Sg[token_of(i)]) == t_key[b];
+              int tot;
+              const int pos = block_excl_count(eq, sh_cnt, &tot) + carry;
+              if (eq && pos == rr) t_vis[b] = i;
+              carry += tot;
+            }
+          }
+          __syncthreads();
+        }
+      }
+      __syncthreads();   // the cleared histogram, the split points
+      fetch_reset();
+      cell_reset();
+      for (int i0 = tid; i0 < N; i0 += kKeyBatch * kThreads) {
+        uint32_t kv[kKeyBatch];
+        fetch(i0, kv);
+#pragma unroll
+        for (int u = 0; u < kKeyBatch; ++u) {
+          const int i = i0 + u * kThreads;
+          if (i < N) {
+            const uint32_t key = kv[u];
+            int bin = 0;
+            for (int b = 0; b < n_t; ++b) {
+              const uint32_t tkb = t_key[b];
+              bin += key > tkb || (key == tkb && (t_eq[b] == 1 || i >= t_vis[b]));
+            }
+            atomicAdd(&hist[bin * ncell + cell_at(i)], 1);
+          }
+        }
+      }
+      __syncthreads();
     } else {
-      // ---- joint histogram of (bin, cell) in visual-token order (the order
-      // the ranking's tie rule refers to): block-wide batches of kThreads
-      // consecutive tokens
+      // ---- joint histogram of (bin, cell) from the cached keys in
+      // visual-token order (the order the ranking's tie rule refers to):
+      // block-wide batches of kThreads consecutive tokens
       for (int i = tid; i < K * ncell; i += kThreads) hist[i] = 0;
       bool any_tie = false;
       for (int b = 0; b < n_t; ++b) any_tie |= (t_eq[b] > 1);
@@ -704,14 +811,13 @@ __device__ __forceinline__ void stats_body(const StatsArgs& a) {
 #pragma unroll
       for (int j = 0; j < 8; ++j) tk[j] = j < n_t ? t_key[j] : 0u;
       __syncthreads();
-      fetch_reset();
       cell_reset();
 #pragma unroll 1
       for (int i0 = 0; i0 < N; i0 += kThreads) {
         {
           const int i = i0 + tid;
           const bool valid = i < N;
-          const uint32_t key = valid ? (cached ? kc[i] : fkey(Sg[token_of(i)])) : 0u;
+          const uint32_t key = valid ? kc[i] : 0u;
           int bin = 0;
           if (!any_tie) {
             if (n_t <= 8) {

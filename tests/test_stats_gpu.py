@@ -145,6 +145,24 @@ def test_many_bins_fine_grid():
     run_stats("K64 M16", [S], sbar, spans, 3, p)
 
 
+def test_many_bins_fine_grid_uncached():
+    """K = 64 bins on a 16 x 16 grid with eight 51x69 frames (N = 28152,
+    more keys than the LDS cache): the unfused joint histogram on keys read
+    from S, with equal keys at several edges split by visual index."""
+    rng = np.random.default_rng(10)
+    spans, Lp = layout(8, 51, 69)
+    is_vis = O.visual_metadata(spans, Lp)[0]
+    vis = np.nonzero(is_vis)[0]
+    S = np.empty((1, 3, Lp), np.float32)
+    S[0, 0] = cluster_row(rng, Lp, vis, 3000, 6000)
+    S[0, 1] = np.where(rng.random(Lp) < 0.4, 1e-3, 4e-3).astype(np.float32)
+    S[0, 2] = rng.lognormal(-7, 1.5, Lp).astype(np.float32)
+    p = sk.params_default()
+    p.n_bins, p.grid = 64, 16
+    sbar = rng.uniform(1e-4, 1e-2, Lp).astype(np.float32)
+    run_stats("K64 M16 uncached", [S, S[:, :, ::-1].copy()], sbar, spans, 8, p, mi_tol=1e-6)
+
+
 @pytest.mark.parametrize("rows,cols,K,M", [(1, 1, 8, 8), (1, 2, 8, 8), (1, 7, 8, 8),
                                             (3, 3, 8, 8), (4, 5, 1, 8), (6, 7, 8, 1),
                                             (9, 11, 64, 16)])
