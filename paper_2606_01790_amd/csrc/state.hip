@@ -204,23 +204,48 @@ __device__ __forceinline__ void stats_body(const StatsArgs& a) {
     const StateHeader* hdr = reinterpret_cast<const StateHeader*>(blk);
     const int nf = a.sp.rows[a.cur] * a.sp.cols[a.cur];
     const bool reset = hdr->nf != nf;
-    // up to four groups per pass: their 12 sums reduce together
+    // up to four groups per pass: their 12 sums reduce together.  One pass
+    // reads the old mean for the sums and writes the new one (element-wise,
+    // each element by one thread), four iterations' loads in flight; a
+    // thread's sums keep ascending token order.
+    constexpr int kU = 4;
     for (int g0 = 0; g0 < a.G; g0 += 4) {
       const int ng = min(4, a.G - g0);
       double acc[12];
 #pragma unroll
       for (int j = 0; j < 12; ++j) acc[j] = 0.0;
-      for (int i = tid; i < nf; i += kThreads) {
+      const float* sg[4];
+      float* mg[4];
 #pragma unroll
-        for (int j = 0; j < 4; ++j) {
-          if (j < ng) {
-            const int gg = g0 + j;
-            const float* m = reinterpret_cast<const float*>(blk + a.m_off) + (size_t)gg * a.frame_cap;
-            const double sv = a.S[(size_t)(layer * a.G + gg) * a.Lp + a.sp.start[a.cur] + i];
-            const double mv = reset ? 0.0 : (double)m[i];
-            acc[3 * j] += sv * mv;
-            acc[3 * j + 1] += sv * sv;
-            acc[3 * j + 2] += mv * mv;
+      for (int j = 0; j < 4; ++j) {
+        const int gg = g0 + min(j, ng - 1);
+        sg[j] = a.S + (size_t)(layer * a.G + gg) * a.Lp + a.sp.start[a.cur];
+        mg[j] = reinterpret_cast<float*>(blk + a.m_off) + (size_t)gg * a.frame_cap;
+      }
+      for (int i0 = tid; i0 < nf; i0 += kU * kThreads) {
+        float sv[kU][4], mv[kU][4];
+#pragma unroll
+        for (int u = 0; u < kU; ++u) {
+          const int i = i0 + u * kThreads;
+#pragma unroll
+          for (int j = 0; j < 4; ++j) {
+            const bool on = j < ng && i < nf;
+            sv[u][j] = on ? sg[j][i] : 0.f;
+            mv[u][j] = (on && !reset) ? mg[j][i] : 0.f;
+          }
+        }
+#pragma unroll
+        for (int u = 0; u < kU; ++u) {
+          const int i = i0 + u * kThreads;
+#pragma unroll
+          for (int j = 0; j < 4; ++j) {
+            if (j < ng && i < nf) {
+              const double sd = sv[u][j], md = mv[u][j];
+              acc[3 * j] += sd * md;
+              acc[3 * j + 1] += sd * sd;
+              acc[3 * j + 2] += md * md;
+              mg[j][i] = a.rho_t * mv[u][j] + (1.f - a.rho_t) * sv[u][j];
+            }
           }
         }
       }
@@ -242,20 +267,7 @@ __device__ __forceinline__ void stats_body(const StatsArgs& a) {
         scal[STARKV_SCAL_PHI(a.G) + g0 + tid] =
             (float)(dot / (sqrt(ns) * sqrt(nm) + (double)a.eps));
       }
-      // the mean update reads the old m above, so every wave is past its sums
-      __syncthreads();
-      for (int i = tid; i < nf; i += kThreads) {
-#pragma unroll
-        for (int j = 0; j < 4; ++j) {
-          if (j < ng) {
-            const int gg = g0 + j;
-            float* m = reinterpret_cast<float*>(blk + a.m_off) + (size_t)gg * a.frame_cap;
-            const float sv = a.S[(size_t)(layer * a.G + gg) * a.Lp + a.sp.start[a.cur] + i];
-            const float mv = reset ? 0.f : m[i];
-            m[i] = a.rho_t * mv + (1.f - a.rho_t) * sv;
-          }
-        }
-      }
+      __syncthreads();   // red12 is reused by the next four groups
     }
     return;
   }
