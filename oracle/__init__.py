@@ -34,5 +34,6 @@ from .starkv_oracle import (  # noqa: F401
     topb_select,
     gather_compact,
     visual_metadata,
+    current_frame_span,
     compress_layer,
 )

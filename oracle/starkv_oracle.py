@@ -401,6 +401,15 @@ def visual_metadata(spans, L_p: int):
     return is_vis, frame, r, c, rows, cols
 
 
+def current_frame_span(spans, F: int):
+    """The span of the current frame F, whose scores form the row s_g^(c)
+    the stability EMA follows (sec. 3.5); None when no span has frame F."""
+    for sp in spans:
+        if sp[3] == F:
+            return sp
+    return None
+
+
 def compress_layer(Q, K, V, L: int, W: int, spans, F: int, B: int,
                    params: Params, state: LayerState, copy_rows=None):
     """One layer of one trajectory step, in the order of Algorithm 1.
@@ -442,9 +451,9 @@ def compress_layer(Q, K, V, L: int, W: int, spans, F: int, B: int,
     # Temporal stability (sec. 3.5): newest frame's tokens, raster order.
     # Reading: a change of the frame's token count restarts m_g from 0; with
     # no visual span at all there is no current row, phi = 0 and m_g stays.
-    spans_f = [sp for sp in spans if sp[3] == F]
-    if spans_f:
-        start, nr, nc, _ = spans_f[0]
+    span_f = current_frame_span(spans, F)
+    if span_f is not None:
+        start, nr, nc, _ = span_f
         n_f = nr * nc
         s_cur = S[:, start:start + n_f]
         m_old = state.m if state.m.shape[1] == n_f else np.zeros((G, n_f))

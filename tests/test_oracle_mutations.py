@@ -122,6 +122,36 @@ def _cells_swapped(r, c, rows, cols, M):
     return (r * M // cols) * M + (c * M // rows)
 
 
+def _metadata(transpose_shape=False, column_major=False):
+    def f(spans, L_p):
+        is_vis = np.zeros(L_p, dtype=bool)
+        frame = np.zeros(L_p, dtype=np.int64)
+        r = np.zeros(L_p, dtype=np.int64)
+        c = np.zeros(L_p, dtype=np.int64)
+        rows = np.ones(L_p, dtype=np.int64)
+        cols = np.ones(L_p, dtype=np.int64)
+        for (start, nr, nc, fr) in spans:
+            if transpose_shape:      # the span's rows and columns swapped
+                nr, nc = nc, nr
+            t = np.arange(start, start + nr * nc)
+            is_vis[t] = True
+            frame[t] = fr
+            if column_major:         # raster walks down the columns
+                r[t] = (t - start) % nr
+                c[t] = (t - start) // nr
+            else:
+                r[t] = (t - start) // nc
+                c[t] = (t - start) % nc
+            rows[t] = nr
+            cols[t] = nc
+        return is_vis, frame, r, c, rows, cols
+    return f
+
+
+def _first_span(spans, F):
+    return spans[0] if spans else None
+
+
 def _prior_raw(mi_bar, tau, eps):
     z = mi_bar / tau
     e = np.exp(z - z.max())
@@ -145,6 +175,15 @@ def _stability_new_mean(s_cur, m, rho_t, eps):
     num = (s_cur * m_new).sum(axis=1)
     den = np.sqrt((s_cur ** 2).sum(axis=1)) * np.sqrt((m_new ** 2).sum(axis=1)) + eps
     return num / den, m_new
+
+
+def _mi_ema_swapped(Q, K, V, L, W, spans, F, B, params, state, copy_rows=None):
+    """compress_layer with the MI EMA weights swapped (rho on the new MI)."""
+    out, st = ORIG["compress_layer"](Q, K, V, L, W, spans, F, B, params, state, copy_rows)
+    rho = params.rho_mi
+    mi_bar = (1.0 - rho) * state.mi_bar + rho * out["mi"]
+    out["mi_bar"] = mi_bar
+    return out, O.LayerState(st.G, mi_bar, st.m, st.n)
 
 
 def _stability_swapped_ema(s_cur, m, rho_t, eps):
@@ -236,9 +275,16 @@ MUTANTS = [
     ("plugin_mi", _mi_log2, "log base 2", MI),
     ("plugin_mi", _mi_swapped_marginals, "wrong bin marginal", MI),
     ("spatial_cells", _cells_swapped, "rows and columns swapped", ["test_spatial_cells_per_frame_grid"]),
+    ("visual_metadata", _metadata(transpose_shape=True), "span rows and columns swapped",
+     ["test_visual_metadata_table"]),
+    ("visual_metadata", _metadata(column_major=True), "column-major raster",
+     ["test_visual_metadata_table"]),
+    ("current_frame_span", _first_span, "stability row from the first span, not frame F's",
+     ["test_stability_row_is_the_current_frame"]),
     ("mi_prior", _prior_raw, "no min-max normalisation", PRIOR),
     ("mi_prior", _prior_negated, "sign of the MI flipped", PRIOR),
     ("lambda_schedule", _lambda_early, "warm-up one step short", ["test_lambda_schedule_values"]),
+    ("compress_layer", _mi_ema_swapped, "MI EMA weights swapped", ["test_mi_ema_closed_form"]),
     ("stability", _stability_new_mean, "phi from the updated mean", STAB),
     ("stability", _stability_swapped_ema, "EMA weights swapped", STAB),
     ("temporal_discount", _discount_sign, "frame distance sign flipped",

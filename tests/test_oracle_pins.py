@@ -258,6 +258,35 @@ def test_spatial_cells_per_frame_grid():
     assert cell[38 * 69] == 56
 
 
+def test_visual_metadata_table():
+    """Sec. 3.1: a frame's rows x cols patch tokens are one raster-ordered
+    run from the span's first token, token start + r*cols + c at row r,
+    column c.  Two non-square spans at non-zero starts (2 rows x 3 columns
+    from token 3, frame 1; 3 rows x 2 columns from token 11, frame 2), with
+    every entry written out by hand."""
+    spans = [(3, 2, 3, 1), (11, 3, 2, 2)]
+    is_vis, frame, r, c, rows, cols = O.visual_metadata(spans, 19)
+    # token:           0  1  2  3  4  5  6  7  8  9 10 11 12 13 14 15 16 17 18
+    want_vis = [0, 0, 0, 1, 1, 1, 1, 1, 1, 0, 0, 1, 1, 1, 1, 1, 1, 0, 0]
+    want_frame = [0, 0, 0, 1, 1, 1, 1, 1, 1, 0, 0, 2, 2, 2, 2, 2, 2, 0, 0]
+    want_r = [0, 0, 0, 0, 0, 0, 1, 1, 1, 0, 0, 0, 0, 1, 1, 2, 2, 0, 0]
+    want_c = [0, 0, 0, 0, 1, 2, 0, 1, 2, 0, 0, 0, 1, 0, 1, 0, 1, 0, 0]
+    want_rows = [1, 1, 1, 2, 2, 2, 2, 2, 2, 1, 1, 3, 3, 3, 3, 3, 3, 1, 1]
+    want_cols = [1, 1, 1, 3, 3, 3, 3, 3, 3, 1, 1, 2, 2, 2, 2, 2, 2, 1, 1]
+    assert is_vis.tolist() == [bool(v) for v in want_vis]
+    assert frame.tolist() == want_frame
+    assert r.tolist() == want_r
+    assert c.tolist() == want_c
+    assert rows.tolist() == want_rows
+    assert cols.tolist() == want_cols
+    # the map feeds the M x M cells of Eq. MI: at M = 2 the 2 x 3 frame's
+    # columns split 0,0,1 (floor(c*2/3)) and its rows 0 | 1
+    vis = np.nonzero(is_vis)[0]
+    cells = O.spatial_cells(r[vis], c[vis], rows[vis], cols[vis], 2)
+    # the 3 x 2 frame's rows split 0,0,1 (floor(r*2/3)) and its columns 0 | 1
+    assert cells.tolist() == [0, 0, 1, 2, 2, 3, 0, 1, 0, 1, 2, 3]
+
+
 def test_mi_empty_token_set():
     assert O.plugin_mi(np.zeros(0, dtype=int), np.zeros(0, dtype=int), 8, 64) == 0.0
 
@@ -297,12 +326,16 @@ def test_lambda_schedule_values():
 
 
 def test_mi_ema_closed_form():
-    """A constant MI c for n steps from zero gives (1 - rho^n) c."""
-    mi_bar = np.zeros(2)
-    c = np.array([0.3, 0.7])
+    """The same layer input on n steps from a fresh state gives the same MI
+    every step, so the EMA from zero (sec. 3.4) closes to (1 - rho^n) MI."""
+    Q, K, V, L, W, spans = _tiny_layer(31)
+    p = O.Params(rho_mi=0.9)
+    st = O.LayerState(2)
     for _ in range(7):
-        mi_bar = 0.9 * mi_bar + 0.1 * c
-    np.testing.assert_allclose(mi_bar, (1 - 0.9 ** 7) * c, rtol=1e-14)
+        out, st = O.compress_layer(Q, K, V, L, W, spans, 1, 5, p, st)
+    assert (out["mi"] > 0).all()
+    np.testing.assert_allclose(out["mi_bar"], (1 - 0.9 ** 7) * out["mi"], rtol=1e-13)
+    assert st.n == 7
 
 
 # ------------------------------------------------------------ stability
@@ -495,6 +528,43 @@ def test_frame_size_change_resets_stability():
     o, st = O.compress_layer(Q2, K2, V2, L2, W2, spans2, 1, 4, p, st)
     np.testing.assert_array_equal(o["phi"], 0.0)
     assert st.m.shape == (2, 15)
+
+
+def test_stability_row_is_the_current_frame():
+    """Sec. 3.5: s_g^(c) is the current frame F's score row.  One query per
+    head and one head per group make S[g] = softmax of one logit row, so a
+    frame whose keys repeat the previous step's frame has a score row
+    proportional to that step's: phi = 1 exactly when the row is taken from
+    frame F.  Step 1 caches frame A; step 2 caches [B (frame 1); A (frame 2)]
+    with F = 2, where B is unrelated, so frame 1's row would give phi < 1."""
+    r = rng(32)
+    G = H = 2
+    W, d, nr, nc, n_text = 1, 8, 2, 3, 4
+    nf = nr * nc
+    A_k = r.standard_normal((G, nf, d)) * 2.0
+    B_k = r.standard_normal((G, nf, d)) * 2.0
+    text = r.standard_normal((G, n_text, d))
+    Q = r.standard_normal((H, W, d))
+    # a negligible epsilon, so that the cosine of parallel rows is 1 to rounding
+    p = O.Params(pool_kernel=1, n_warmup=0, n_ramp=0, eps=1e-30)
+    K1 = np.concatenate([A_k, text], axis=1)
+    o1, st = O.compress_layer(Q, K1, K1, nf + n_text, W, [(0, nr, nc, 1)], 1, 3, p,
+                              O.LayerState(G))
+    K2 = np.concatenate([B_k, A_k, text], axis=1)
+    spans2 = [(0, nr, nc, 1), (nf, nr, nc, 2)]
+    o2, st = O.compress_layer(Q, K2, K2, 2 * nf + n_text, W, spans2, 2, 3, p, st)
+    np.testing.assert_allclose(o2["phi"], 1.0, rtol=0, atol=1e-12)
+    # the rows themselves: frame A's scores scale by the softmax normaliser
+    ratio = o2["S"][:, nf:2 * nf] / o1["S"][:, :nf]
+    np.testing.assert_allclose(ratio, ratio[:, :1] * np.ones((1, nf)), rtol=1e-12)
+    # the EMA from zero after two steps: 0.09 * step-1 row + 0.1 * step-2 row
+    np.testing.assert_allclose(st.m, 0.09 * o1["S"][:, :nf] + 0.1 * o2["S"][:, nf:2 * nf],
+                               rtol=1e-14)
+    # frame 1's row at step 2 is not parallel to step 1's row
+    b = o2["S"][:, :nf]
+    a = o1["S"][:, :nf]
+    cos = (a * b).sum(1) / np.sqrt((a * a).sum(1) * (b * b).sum(1))
+    assert (cos < 0.999).all()
 
 
 # ----------------------------------------------- decode over the cache (4.3)
