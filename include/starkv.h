@@ -21,7 +21,8 @@
  *  - Pointers named as device pointers must be device memory.  Host
  *    pointers (dims, params, layouts, spans) are read only during the call.
  *  - The caller owns every buffer.  The library keeps no pointer after a
- *    call returns and has no global mutable state.
+ *    call returns and has no global mutable state, except the device array
+ *    behind starkv_score_noalloc (see there).
  *  - All arguments are validated on the host before any GPU work is queued.
  *    On any error code nothing is written and nothing is launched.
  *  - Tokens are 0-based.  L is the cache length of the step, W the
@@ -234,6 +235,27 @@ starkv_status starkv_score(const starkv_dims* dims, const starkv_params* params,
                            const starkv_kv_layout* k_layout,
                            float* S, float* sbar, uint8_t* gstar,
                            void* ws, size_t ws_bytes, void* stream);
+
+/* starkv_score for callers that cannot allocate device memory: code under
+ * HIP graph capture, tight serving loops, harnesses that forbid hipMalloc.
+ * Same arguments, computation and results as starkv_score, without ws: the
+ * workspace is a library-owned device array of STARKV_NOALLOC_SCRATCH_BYTES
+ * that every GPU the library runs on holds from module load until the
+ * process ends (one copy per device).  The call allocates nothing; its
+ * first call on a device looks up that device's copy (no allocation).
+ * Calls that overlap on one GPU (other streams, other host threads) share
+ * the array and race: order them, or use starkv_score with separate
+ * workspaces.  The array keeps the last call's contents; the call needs no
+ * clearing of it.
+ * Errors: as starkv_score, with E_WORKSPACE when
+ * starkv_workspace_bytes(dims) > STARKV_NOALLOC_SCRATCH_BYTES. */
+#define STARKV_NOALLOC_SCRATCH_BYTES ((size_t)64 << 20)
+starkv_status starkv_score_noalloc(const starkv_dims* dims,
+                                   const starkv_params* params,
+                                   const void* q, const void* k,
+                                   const starkv_kv_layout* k_layout,
+                                   float* S, float* sbar, uint8_t* gstar,
+                                   void* stream);
 
 /* Online statistics of one step (sec. 3.4 online MI prior, sec. 3.5
  * stability, sec. 3.6 entropy and temperature; Algorithm 1, MI and AEB

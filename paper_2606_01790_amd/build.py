@@ -15,7 +15,7 @@ LIB = os.path.join(PKG, "libstarkv.so")
 INCLUDE = os.path.join(ROOT, "include")
 
 HIP_SOURCES = ["score.hip", "score_bf16.hip", "score_f32.hip", "state.hip", "select.hip",
-               "compact.hip", "decode.hip"]
+               "compact.hip", "decode.hip", "noalloc.hip"]
 HOST_SOURCES = ["validate.cpp", "api.cpp"]
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")

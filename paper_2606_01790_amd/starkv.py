@@ -85,6 +85,9 @@ SIGNATURES = {
     "starkv_score": (c_int32, [POINTER(Dims), POINTER(Params), c_void_p, c_void_p,
                                POINTER(KVLayout), c_void_p, c_void_p, c_void_p,
                                c_void_p, c_size_t, c_void_p]),
+    "starkv_score_noalloc": (c_int32, [POINTER(Dims), POINTER(Params), c_void_p, c_void_p,
+                                       POINTER(KVLayout), c_void_p, c_void_p, c_void_p,
+                                       c_void_p]),
     "starkv_update_state": (c_int32, [POINTER(Dims), POINTER(Params), c_void_p,
                                       c_void_p, POINTER(Span), c_int32, c_int32,
                                       c_void_p, c_int32, c_void_p, c_void_p,
@@ -220,6 +223,20 @@ def score(dims: Dims, params: Params, q, k, k_layout: KVLayout, S, sbar, gstar,
         ctypes.byref(dims), ctypes.byref(params), _ptr(q), _ptr(k),
         ctypes.byref(k_layout), _ptr(S), _ptr(sbar), _ptr(gstar), _ptr(ws),
         ws.numel() * ws.element_size(), _stream(stream)))
+
+
+def score_noalloc(dims: Dims, params: Params, q, k, k_layout: KVLayout, S, sbar, gstar,
+                  stream=None):
+    """starkv_score with the library's own device workspace (no ws)."""
+    nl, Lp = dims.n_layers, dims.Lp
+    _need(q, nl * dims.H * dims.W * dims.d * _esz(dims), "q")
+    _need_cache(k, dims, k_layout, "k")
+    _need(S, nl * dims.Ns * Lp * 4, "S")
+    _need(sbar, nl * Lp * 4, "sbar")
+    _need(gstar, nl * Lp, "gstar")
+    _check("starkv_score_noalloc", lib().starkv_score_noalloc(
+        ctypes.byref(dims), ctypes.byref(params), _ptr(q), _ptr(k),
+        ctypes.byref(k_layout), _ptr(S), _ptr(sbar), _ptr(gstar), _stream(stream)))
 
 
 def update_state(dims: Dims, params: Params, S, sbar, spans, frame: int, state,

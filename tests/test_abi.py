@@ -32,7 +32,7 @@ def declared_functions():
 def test_header_symbols_are_exported():
     L = sk.lib()
     names = declared_functions()
-    assert len(names) == 13
+    assert len(names) == 14
     for n in names:
         assert hasattr(L, n), n
     assert set(names) == set(sk.SIGNATURES)
@@ -234,3 +234,20 @@ def test_decode_validation_and_workspace():
     assert ws == (28 * 4 * 11 * 7 * 130 * 4 + 255) // 256 * 256
     assert _decode(d, n=2723, ws_bytes=ws - 1) == "E_WORKSPACE"
     assert sk.decode_workspace_bytes(d, 0) == 0
+
+
+def test_noalloc_rejects_workspace_beyond_its_array():
+    """starkv_score_noalloc checks its workspace need against the library's
+    array on the host: a 200000-token, W = 64 step needs more than 64 MiB."""
+    dims = sk.make_dims(28, 28, 4, 128, 200000, 64, sk.BF16)
+    assert sk.workspace_bytes(dims) > 64 << 20
+    lay = sk.KVLayout(4 * 200000 * 128, 200000 * 128, 128)
+    code = sk.lib().starkv_score_noalloc(
+        ctypes.byref(dims), ctypes.byref(sk.params_default()), FAKE, FAKE,
+        ctypes.byref(lay), FAKE, FAKE, FAKE, None)
+    assert sk.STATUS[code] == "E_WORKSPACE"
+    small = sk.make_dims(1, 4, 2, 64, 256, 8, sk.F32)
+    code = sk.lib().starkv_score_noalloc(
+        ctypes.byref(small), ctypes.byref(sk.params_default()), None, FAKE,
+        ctypes.byref(sk.KVLayout(2 * 256 * 64, 256 * 64, 64)), FAKE, FAKE, FAKE, None)
+    assert sk.STATUS[code] == "E_NULL"
