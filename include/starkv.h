@@ -277,9 +277,16 @@ starkv_status starkv_score_noalloc(const starkv_dims* dims,
  *          frame F (must be a span's frame when n_spans > 0).
  * state:   device, from starkv_state_init with the same dims and frame_cap;
  *          the current frame's rows*cols must be <= frame_cap (E_STATE).
+ *          The state lives in device memory, so the host cannot check it: a
+ *          layer whose state block was not initialised for the same
+ *          subspace count and frame_cap is left untouched and gets NaN in
+ *          all of its scalars.  (A frame_cap above the one the buffer was
+ *          sized for addresses memory past the buffer; it is the caller's
+ *          to match the allocation.)
  * scalars: device out, float32 [n_layers][starkv_scalars_count(dims)].
+ * ws, ws_bytes: unused (reserved); may be NULL and 0.
  * Every per-group quantity above is per subspace (Ns of them).
- * Errors: E_NULL, E_SHAPE, E_SPANS, E_PARAM, E_STATE, E_WORKSPACE, E_HIP. */
+ * Errors: E_NULL, E_SHAPE, E_SPANS, E_PARAM, E_STATE, E_ALIGN, E_HIP. */
 starkv_status starkv_update_state(const starkv_dims* dims,
                                   const starkv_params* params,
                                   const float* S, const float* sbar,
@@ -299,7 +306,8 @@ starkv_status starkv_update_state(const starkv_dims* dims,
  * starkv_update_state; spans/frame as for starkv_update_state.
  * s:   device out, float32 [n_layers][L_p].
  * idx: device out, int32 [n_layers][B] (may be NULL when B == 0).
- * Errors: E_NULL, E_SHAPE, E_BUDGET, E_SPANS, E_PARAM, E_WORKSPACE, E_HIP. */
+ * ws, ws_bytes: unused (reserved); may be NULL and 0.
+ * Errors: E_NULL, E_SHAPE, E_BUDGET, E_SPANS, E_PARAM, E_ALIGN, E_HIP. */
 starkv_status starkv_select(const starkv_dims* dims, const starkv_params* params,
                             const float* sbar, const uint8_t* gstar,
                             const float* scalars,
@@ -312,7 +320,10 @@ starkv_status starkv_select(const starkv_dims* dims, const starkv_params* params
  *   K'[g] = [K[g, idx[0..B)]; K[g, L_p..L)],  V' likewise.
  * k, v:   device caches with layout *kv_layout (both use it), dims->dtype.
  * idx:    device, int32 [n_layers][B], every entry in [0, L_p); ascending
- *         order is what starkv_select writes but is not required.
+ *         order is what starkv_select writes but is not required.  The
+ *         kernel never reads outside the cache: an entry outside [0, L_p)
+ *         (a caller bug) produces an all-zero row in K' and V' instead of a
+ *         copy, so check idx before relying on rows that come out zero.
  * k_out, v_out: device out, [n_layers][G][B + W][d] contiguous, bit copies.
  * Outputs must not overlap the inputs.
  * Errors: E_NULL, E_SHAPE, E_DTYPE, E_ALIGN, E_BUDGET, E_HIP. */

@@ -124,12 +124,54 @@ struct KStage {
   static constexpr bool may_pass(int j) { return (kRowStep - 1) + j * kRowStep >= kRows; }
 };
 
-// Tile staging, written inline in each kernel over a local array so that the
-// staging vectors stay in registers; every load and store is unconditional.
-// `full`: the tile's rows all lie before Lp, so no token index is clamped and
-// the addresses step by a uniform stride.
-#define STARKV_STAGE_FETCH(KS, NTH, r, kg, ts, t0, Lp, full)                       {                                                                                  const int r0_ = (int)threadIdx.x / KS::kVecPerRow;                               const int c0_ = ((int)threadIdx.x % KS::kVecPerRow) * KS::kElemPerVec;           if (full) {                                                                        const auto* p_ = (kg) + (int64_t)((t0) + r0_) * (ts) + c0_;                      _Pragma("unroll") for (int j_ = 0; j_ < KS::kPerThread; ++j_) {                    if (KS::may_pass(j_)) {                                                            const int row_ = min(r0_ + j_ * KS::kRowStep, KS::kRows - 1);                    r[j_] = *reinterpret_cast<const i32x4*>((kg) + (int64_t)((t0) + row_) * (ts) + c0_);         } else {                                                                           r[j_] = *reinterpret_cast<const i32x4*>(p_ + (int64_t)(j_ * KS::kRowStep) * (ts));         }                                                                              }                                                                              } else {                                                                           _Pragma("unroll") for (int j_ = 0; j_ < KS::kPerThread; ++j_) {                    const int row_ = min(r0_ + j_ * KS::kRowStep, KS::kRows - 1);                    const int tok_ = min((t0) + row_, (Lp) - 1);                                     r[j_] = *reinterpret_cast<const i32x4*>((kg) + (int64_t)tok_ * (ts) + c0_);       }                                                                              }                                                                              }
-#define STARKV_STAGE_STORE(KS, NTH, r, buf)                                        {                                                                                  const int r0_ = (int)threadIdx.x / KS::kVecPerRow;                               const int c0_ = ((int)threadIdx.x % KS::kVecPerRow) * KS::kElemPerVec;           auto* q_ = (buf) + r0_ * KS::kStride + c0_;                                      _Pragma("unroll") for (int j_ = 0; j_ < KS::kPerThread; ++j_) {                    if (KS::may_pass(j_)) {                                                            const int row_ = min(r0_ + j_ * KS::kRowStep, KS::kRows - 1);                    *reinterpret_cast<i32x4*>((buf) + row_ * KS::kStride + c0_) = r[j_];           } else {                                                                           *reinterpret_cast<i32x4*>(q_ + j_ * KS::kRowStep * KS::kStride) = r[j_];       }                                                                              }                                                                              }
+// Tile staging.  stage_fetch loads the 16-byte vectors a thread stages of
+// the tile of rows t0 .. t0+127 into registers; stage_store writes them to
+// an LDS tile buffer.  Every load and store is unconditional: rows past the
+// tile repeat its last row, and with `full` false (the tile reaches past
+// L_p) tokens are clamped to L_p - 1.  With `full` true every row lies
+// before L_p, so the addresses step by one uniform stride.  Both are forced
+// inline so that the staging array stays in registers.
+template <typename KS, typename T>
+__device__ __forceinline__ void stage_fetch(i32x4 (&r)[KS::kPerThread], const T* kg,
+                                            int64_t ts, int t0, int Lp, bool full) {
+  const int r0 = (int)threadIdx.x / KS::kVecPerRow;
+  const int c0 = ((int)threadIdx.x % KS::kVecPerRow) * KS::kElemPerVec;
+  if (full) {
+    const T* p = kg + (int64_t)(t0 + r0) * ts + c0;
+#pragma unroll
+    for (int j = 0; j < KS::kPerThread; ++j) {
+      if (KS::may_pass(j)) {
+        const int row = min(r0 + j * KS::kRowStep, KS::kRows - 1);
+        r[j] = *reinterpret_cast<const i32x4*>(kg + (int64_t)(t0 + row) * ts + c0);
+      } else {
+        r[j] = *reinterpret_cast<const i32x4*>(p + (int64_t)(j * KS::kRowStep) * ts);
+      }
+    }
+  } else {
+#pragma unroll
+    for (int j = 0; j < KS::kPerThread; ++j) {
+      const int row = min(r0 + j * KS::kRowStep, KS::kRows - 1);
+      const int tok = min(t0 + row, Lp - 1);
+      r[j] = *reinterpret_cast<const i32x4*>(kg + (int64_t)tok * ts + c0);
+    }
+  }
+}
+
+template <typename KS, typename T>
+__device__ __forceinline__ void stage_store(const i32x4 (&r)[KS::kPerThread], T* buf) {
+  const int r0 = (int)threadIdx.x / KS::kVecPerRow;
+  const int c0 = ((int)threadIdx.x % KS::kVecPerRow) * KS::kElemPerVec;
+  T* q = buf + r0 * KS::kStride + c0;
+#pragma unroll
+  for (int j = 0; j < KS::kPerThread; ++j) {
+    if (KS::may_pass(j)) {
+      const int row = min(r0 + j * KS::kRowStep, KS::kRows - 1);
+      *reinterpret_cast<i32x4*>(buf + row * KS::kStride + c0) = r[j];
+    } else {
+      *reinterpret_cast<i32x4*>(q + j * KS::kRowStep * KS::kStride) = r[j];
+    }
+  }
+}
 
 // Q fragments of the 32 window rows a wave owns (row block `wave` of the
 // group), held in registers for the whole kernel; rows past R are zero.
@@ -171,8 +213,8 @@ __global__ __launch_bounds__(NRB * 64) void score_pass1(ScoreArgs a) {
   typename M::frag qf[NK];
   load_q_frags<T, D>(group_q<T, D>(a, layer, g), a.R, wave, qf);
   i32x4 sr[KS::kPerThread];
-  STARKV_STAGE_FETCH(KS, NRB * 64, sr, kg, a.ts, t_begin, a.Lp, t_begin + KS::kRows <= a.Lp)
-  STARKV_STAGE_STORE(KS, NRB * 64, sr, kbuf)
+  stage_fetch<KS>(sr, kg, a.ts, t_begin, a.Lp, t_begin + KS::kRows <= a.Lp);
+  stage_store<KS>(sr, kbuf);
   __syncthreads();
 
   // (m, l): reference logit and sum of 2^((y - m) * log2e/sqrt(d)) of the
@@ -232,7 +274,7 @@ __global__ __launch_bounds__(NRB * 64) void score_pass1(ScoreArgs a) {
   int buf = 0;
   for (int t0 = t_begin; t0 < t_end; t0 += KS::kRows) {
     const bool more = t0 + KS::kRows < t_end;
-    if (more) { STARKV_STAGE_FETCH(KS, NRB * 64, sr, kg, a.ts, t0 + KS::kRows, a.Lp, t0 + 2 * KS::kRows <= a.Lp) }
+    if (more) stage_fetch<KS>(sr, kg, a.ts, t0 + KS::kRows, a.Lp, t0 + 2 * KS::kRows <= a.Lp);
     const T* tile = kbuf + buf * KS::kElems;
     if (t0 + KS::kRows <= t_end) {
       // full tile: branch-free, the MFMA chain of block b+1 is issued before
@@ -254,7 +296,7 @@ __global__ __launch_bounds__(NRB * 64) void score_pass1(ScoreArgs a) {
         }
       }
     }
-    if (more) { STARKV_STAGE_STORE(KS, NRB * 64, sr, kbuf + (buf ^ 1) * KS::kElems) }
+    if (more) stage_store<KS>(sr, kbuf + (buf ^ 1) * KS::kElems);
     __syncthreads();
     buf ^= 1;
   }
@@ -324,14 +366,14 @@ __global__ __launch_bounds__(NRB * 64) void score_pass2(ScoreArgs a) {
 
   __shared__ __align__(16) float cs[NRB * 32];
   i32x4 sr[KS::kPerThread];
-  STARKV_STAGE_FETCH(KS, NRB * 64, sr, kg, a.ts, t_begin, a.Lp, t_begin + KS::kRows <= a.Lp)
+  stage_fetch<KS>(sr, kg, a.ts, t_begin, a.Lp, t_begin + KS::kRows <= a.Lp);
   typename M::frag qf[NK];
   load_q_frags<T, D>(group_q<T, D>(a, layer, g), a.R, wave, qf);
   {
     const float2* part = a.part + (size_t)(layer * a.G + g) * a.n_chunks_max * a.Rpad;
     for (int r = threadIdx.x; r < NRB * 32; r += NRB * 64) cs[r] = merge_row(a, part, r);
   }
-  STARKV_STAGE_STORE(KS, NRB * 64, sr, kbuf)
+  stage_store<KS>(sr, kbuf);
   __syncthreads();
   // c of the rows this lane receives: wave*32 + 8i + 4*half + j
   float c[16];
@@ -345,7 +387,7 @@ __global__ __launch_bounds__(NRB * 64) void score_pass2(ScoreArgs a) {
   int buf = 0;
   for (int t0 = t_begin; t0 < t_end; t0 += KS::kRows) {
     const bool more = t0 + KS::kRows < t_end;
-    if (more) { STARKV_STAGE_FETCH(KS, NRB * 64, sr, kg, a.ts, t0 + KS::kRows, a.Lp, t0 + 2 * KS::kRows <= a.Lp) }
+    if (more) stage_fetch<KS>(sr, kg, a.ts, t0 + KS::kRows, a.Lp, t0 + 2 * KS::kRows <= a.Lp);
     const T* tile = kbuf + buf * KS::kElems;
     float* rs = red + buf * (NRB * n_part * KS::kRows);
 #pragma unroll
@@ -376,7 +418,7 @@ __global__ __launch_bounds__(NRB * 64) void score_pass2(ScoreArgs a) {
         }
       }
     }
-    if (more) { STARKV_STAGE_STORE(KS, NRB * 64, sr, kbuf + (buf ^ 1) * KS::kElems) }
+    if (more) stage_store<KS>(sr, kbuf + (buf ^ 1) * KS::kElems);
     __syncthreads();
     if (!SUB) {           // one subspace per group: all NRB wave sums
       for (int i = threadIdx.x; i < KS::kRows; i += NRB * 64) {

@@ -34,6 +34,7 @@
 // so that the binning pass itself reads in any order with loads in flight.
 // Either way ties resolve exactly as the ranking defines.
 #include "device_common.h"
+#include "grid_cell.h"
 #include "internal.h"
 
 namespace starkv {
@@ -85,16 +86,6 @@ static_assert(63 * kTieChunks <= kKeyCache, "tie-split counts live in the key ca
 constexpr size_t kStatsLds =
     (size_t)kHistInts * 4 + (size_t)kKeyCache * 4 + (size_t)kCand * 4;
 
-// floor(x * M / n) without an integer division, for 0 <= x < 2^22 and
-// x * M < 2^31: the float estimate is within one of the quotient, and one
-// correction step makes it exact.
-__device__ inline int scaled_index(int x, int M, int n, float m_over_n) {
-  int q = (int)((float)x * m_over_n);
-  const int xm = x * M;
-  if (q * n > xm) --q;
-  else if ((q + 1) * n <= xm) ++q;
-  return q;
-}
 
 // Sum over the wave's lanes (integers: exact in any order).
 __device__ inline int wave_sum_i(int v) {
@@ -358,9 +349,7 @@ __device__ __forceinline__ void stats_body(const StatsArgs& a) {
         q_rows = sp_rows[q_s];
         q_cols = sp_cols[q_s];
         q_end = sp_off[q_s + 1];
-        const int p = i - sp_off[q_s];
-        q_r = scaled_index(p, 1, q_cols, 1.0f / (float)q_cols);   // p / cols
-        q_c = p - q_r * q_cols;
+        span_row_col(i - sp_off[q_s], q_cols, &q_r, &q_c);
         q_dq = kThreads / q_cols;
         q_dr = kThreads - q_dq * q_cols;
         q_fr = (float)M / (float)q_rows;
@@ -371,7 +360,7 @@ __device__ __forceinline__ void stats_body(const StatsArgs& a) {
         if (q_c >= q_cols) { q_c -= q_cols; ++q_r; }
       }
       q_next = i + kThreads;
-      return scaled_index(q_r, M, q_rows, q_fr) * M + scaled_index(q_c, M, q_cols, q_fc);
+      return grid_cell(q_r, q_c, q_rows, q_cols, M, q_fr, q_fc);
     };
     auto cell_reset = [&]() { q_s = 0; q_next = -1; };
 
@@ -940,9 +929,20 @@ __device__ __forceinline__ void finalize_layer(const FinalArgs& a, int layer, in
 // clears the count.  No block waits for another.
 __global__ __launch_bounds__(kThreads) void stats_kernel(StatsArgs a) {
   __shared__ int last_s;
-  stats_body(a);
   const int layer = blockIdx.y;
   StateHeader* hdr = reinterpret_cast<StateHeader*>(a.state + (size_t)layer * a.state_stride);
+  // A state block built for other dimensions (another subspace count or
+  // frame capacity, or never initialised) is left untouched: the layer's
+  // scalars become NaN and no block reads or writes its statistics.  The
+  // checked fields are written only by starkv_state_init, so reading them
+  // here races with nothing.
+  if (hdr->magic != kStateMagic || hdr->G != a.G || hdr->frame_cap != a.frame_cap) {
+    if (blockIdx.x == 0)
+      for (int i = threadIdx.x; i < a.sc; i += kThreads)
+        a.scal[(size_t)layer * a.sc + i] = __builtin_nanf("");
+    return;
+  }
+  stats_body(a);
   // Thread 0 wrote every value the finalize reads (MI_g or H^); its fence
   // publishes them before it counts the block.
   __syncthreads();

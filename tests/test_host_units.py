@@ -1,0 +1,79 @@
+"""Host-side units built with the host compiler (no GPU, no HIP).
+
+1. The C ABI's validation layer (validate.cpp, api.cpp) under the address
+   and undefined-behaviour sanitizers, with stub kernel launches: every
+   status code of include/starkv.h comes back where the header says.
+2. The spatial-cell arithmetic of the statistics kernel (grid_cell.h, the
+   same source the kernel compiles) against exact integer arithmetic, up to
+   the largest frames the boundary accepts (rows * cols <= 2^26).
+"""
+
+import os
+import random
+import shutil
+import subprocess
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+CSRC = os.path.join(ROOT, "paper_2606_01790_amd", "csrc")
+INC = os.path.join(ROOT, "include")
+HOST = os.path.join(ROOT, "tests", "host")
+
+pytestmark = pytest.mark.skipif(shutil.which("g++") is None, reason="no host compiler")
+
+
+def _build(tmp_path, name, sources, sanitize):
+    exe = str(tmp_path / name)
+    cmd = ["g++", "-std=c++17", "-g", "-O1", f"-I{INC}", f"-I{CSRC}", *sources, "-o", exe]
+    if sanitize:
+        cmd[1:1] = ["-fsanitize=address,undefined", "-fno-sanitize-recover=all",
+                    "-fno-omit-frame-pointer"]
+    r = subprocess.run(cmd, capture_output=True, text=True)
+    assert r.returncode == 0, r.stderr
+    return exe
+
+
+def test_abi_validation_under_sanitizers(tmp_path):
+    exe = _build(tmp_path, "abi_driver",
+                 [os.path.join(HOST, "abi_driver.cpp"), os.path.join(CSRC, "validate.cpp"),
+                  os.path.join(CSRC, "api.cpp")], sanitize=True)
+    env = dict(os.environ, ASAN_OPTIONS="detect_leaks=1", UBSAN_OPTIONS="print_stacktrace=1")
+    r = subprocess.run([exe], capture_output=True, text=True, env=env, timeout=120)
+    assert r.returncode == 0, r.stdout[-2000:] + r.stderr[-2000:]
+    assert "checks passed" in r.stdout
+    codes = {int(line.rsplit("-> ", 1)[1]) for line in r.stdout.splitlines()
+             if line.startswith("ok ") and "status string" not in line
+             and "launch count" not in line and "bytes" not in line
+             and "count" not in line}
+    # every starkv_status value 0..10 occurs
+    assert set(range(11)) <= codes, sorted(codes)
+
+
+def _cells(exe, cases):
+    inp = "".join(f"{p} {rows} {cols} {M}\n" for p, rows, cols, M in cases)
+    r = subprocess.run([exe], input=inp, capture_output=True, text=True, timeout=120)
+    assert r.returncode == 0, r.stderr
+    return [tuple(map(int, line.split())) for line in r.stdout.splitlines()]
+
+
+def test_grid_cells_exact_at_large_positions(tmp_path):
+    exe = _build(tmp_path, "grid_cell_driver", [os.path.join(HOST, "grid_cell_driver.cpp")],
+                 sanitize=True)
+    rnd = random.Random(5)
+    cases = []
+    big = 1 << 26                                   # largest span the boundary accepts
+    for rows, cols in [(big, 1), (big // 2, 2), (big // 3, 3), (1, big), (8191, 8192),
+                       (4096 * 4, 4096), (39, 69), (51, 91), (4000, 4000), (3, big // 3)]:
+        n = rows * cols
+        for M in (1, 7, 8, 16):
+            pts = {0, n - 1, n // 2, n // 3, min(n - 1, 33554434), min(n - 1, (1 << 25) - 1)}
+            pts |= {rnd.randrange(n) for _ in range(40)}
+            cases += [(p, rows, cols, M) for p in sorted(pts)]
+    got = _cells(exe, cases)
+    assert len(got) == len(cases)
+    for (p, rows, cols, M), (r, c, cell) in zip(cases, got):
+        assert (r, c) == divmod(p, cols), (p, rows, cols)
+        want = (r * M // rows) * M + (c * M // cols)
+        assert cell == want, (p, rows, cols, M, cell, want)
+        assert 0 <= cell < M * M
