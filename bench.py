@@ -180,8 +180,8 @@ def call_bytes(spec, s, name, per_head=False):
     e, nl, H, G, d, W = sp.elem_bytes, sp.n_layers, sp.H, sp.G, sp.d, sp.W
     Ns = H if per_head else G
     Lp, nv, nf, B = sp.L_p(s), sp.n_vis(s), sp.n_frame, sp.budgets(s)[0]
-    if name == "score":        # Q, K_past in; S, sbar, g* out
-        per = e * (H * W * d + G * Lp * d) + 4 * Ns * Lp + 4 * Lp + Lp
+    if name == "score":        # Q and K_past read once (S, sbar, g* are intermediates)
+        per = e * (H * W * d + G * Lp * d)
     elif name == "update_state":   # S of visual tokens, sbar, stability means
         per = 4 * Ns * nv + 4 * Lp + 4 * Ns * nf * 3
     elif name == "select":     # sbar, g* in; s, idx out
@@ -338,6 +338,7 @@ def main():
                          "alg_flops_per_launch": int(avg_f)})
         per_call_us = {n: round(per[n]["time"] / per[n]["launches"] * 1e6, 2) for n in per}
 
+    copy_gbs = measure_copy_bandwidth(torch)
     cpu = None
     if not args.no_cpu_baseline:
         cpu = cpu_baseline(spec, params, args.cpu_seconds, args.per_head, args.tem_decay,
@@ -367,6 +368,8 @@ def main():
                    + (f", {args.groups} layer groups on {args.groups} streams"
                       if args.groups > 1 else "")},
         "hbm_frac_path": round(bytes_alg / (ms_per_step * 1e-3) / (HBM_PEAK_GBS * 1e9), 4),
+        "copy_gbs_measured": round(copy_gbs, 1),
+        "copy_frac_path": round(bytes_alg / (ms_per_step * 1e-3) / (copy_gbs * 1e9), 4),
         "per_call_us": per_call_us,
         "roofline": roofline,
         "cpu_baseline": cpu,
@@ -447,6 +450,7 @@ def decode_bench(args):
                      "attention_mflops_per_token": round(nl * WL.decode_flops(H, n, d) / 1e6, 2)}
     comp, full = res["compressed"], res["full"]
     t_c = comp["us_per_token"] * 1e-6
+    copy_gbs = measure_copy_bandwidth(torch)
     cpu = None
     if not args.no_cpu_baseline:
         cpu = decode_cpu_baseline(spec, r, q, n_c, args.cpu_seconds)
@@ -506,6 +510,7 @@ def decode_cpu_baseline(spec, runner, q, n_c, seconds):
         spent += time.perf_counter() - t0
         layers += 1
     return {"value": round(layers / nl / spent, 1), "unit": "tokens/s", "cores": blas_threads(),
+            **host_info(),
             "kind": "oracle",
             "sample": f"{layers} layer decodes over the compressed caches of {spec.name} "
                       f"(step {spec.steps}, {n_c} tokens per group; {spent:.1f} s of oracle "
@@ -514,7 +519,8 @@ def decode_cpu_baseline(spec, runner, q, n_c, seconds):
 
 # Sources whose kernels the committed traffic figure was measured on.
 TRAFFIC_SOURCES = {
-    "starkv_score": ["score_kernels.h", "score.hip", "score_bf16.hip", "device_common.h"],
+    "starkv_score": ["score_kernels.h", "score_slab.h", "score.hip", "score_bf16.hip",
+                     "device_common.h"],
 }
 
 
@@ -546,6 +552,44 @@ def measured_traffic(call, workload):
         return int(vals["traffic_bytes_per_launch"])
     except (KeyError, ValueError):
         return None
+
+
+def measure_copy_bandwidth(torch, reps=5):
+    """Device-to-device copy rate of this GPU (GB/s, bytes read plus bytes
+    written): 1 GiB copied with torch's copy kernel, best of `reps`, timed
+    with HIP events on the current stream."""
+    n = 1 << 28
+    a = torch.ones(n, dtype=torch.float32, device="cuda")
+    b = torch.empty_like(a)
+    b.copy_(a)
+    torch.cuda.synchronize()
+    stream = torch.cuda.current_stream()
+    best = float("inf")
+    for _ in range(reps):
+        e0 = torch.cuda.Event(enable_timing=True)
+        e1 = torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        b.copy_(a)
+        e1.record(stream)
+        torch.cuda.synchronize()
+        best = min(best, e0.elapsed_time(e1) * 1e-3)
+    del a, b
+    return 2 * 4 * n / best / 1e9
+
+
+def host_info():
+    """Cores this process may run on, the CPU model, and the BLAS threads."""
+    model = "unknown"
+    try:
+        with open("/proc/cpuinfo") as fh:
+            for ln in fh:
+                if ln.startswith("model name"):
+                    model = ln.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
+    return {"affinity_cores": len(os.sched_getaffinity(0)), "cpu_model": model,
+            "blas_threads": blas_threads()}
 
 
 def blas_threads():
@@ -595,7 +639,7 @@ def cpu_baseline(spec, params, seconds, per_head=False, tem_decay="exp", aeb="en
         runs += 1
         layer = (layer + 1) % spec.n_layers
     return {"value": round(tokens / spent, 1), "unit": "layer-tokens/s", "cores": threads,
-            "kind": "oracle",
+            "kind": "oracle", **host_info(),
             "sample": f"{runs} whole {spec.steps}-step layer trajectories of {spec.name} "
                       + ("with per-head subspaces " if per_head else "")
                       + f"(layers 0-{min(runs, spec.n_layers) - 1}; {tokens} layer-tokens, "

@@ -15,6 +15,20 @@ The bar (per layer and step):
 Decisions (rank bins, top-B) are re-taken by the oracle on the GPU's own
 float32 values for the stage-wise checks, so both sides decide on identical
 numbers.
+
+Near ties (end to end only; the stage-wise checks above stay exact):
+  * rank bins: a visual token whose oracle S lies within 1e-3 relative of
+    the oracle's S at a bin edge may fall in either adjacent bin, since S
+    is only fixed to that tolerance.  Every token that the GPU's S and the
+    oracle's S bin differently must be such a token, moved by one bin; then
+    the end-to-end MI may differ from the oracle's by as much as the
+    oracle's own MI on the two score sets differs (plus the 2e-3 bound),
+    and MI_bar by (1 - rho_mi) of that excess;
+  * the min-max prior (sec. 3.4) is ill-conditioned when the spread of the
+    subspaces' MI_bar is within 100x the GPU-oracle MI_bar difference (with
+    two subspaces min-max maps them to 0 and 1 whatever their gap): w is
+    then not fixed by the tolerance, and the end-to-end fused score is the
+    oracle's fusion taken with the GPU's w (itself checked stage-wise).
 """
 
 from __future__ import annotations
@@ -60,6 +74,38 @@ def topb_band_ok(idx_gpu, s_or, B):
     return bool(ok), int(diff.size)
 
 
+def near_tie_bin_moves(v_or, v_gpu, K):
+    """Tokens whose rank bin differs between the oracle's scores v_or and the
+    GPU's v_gpu (the same visual tokens), if every one of them is a near tie
+    at a bin edge: moved by one bin, with its oracle score within REL of the
+    oracle's score at the edge between the two bins.  Returns the count, or
+    None if some move is not explained by a near tie."""
+    v_or = np.asarray(v_or, np.float64)
+    N = v_or.shape[0]
+    if N == 0 or K <= 1:
+        return 0
+    b_or = O.rank_bins(v_or, K)
+    b_g = O.rank_bins(np.asarray(v_gpu, np.float64), K)
+    moved = np.nonzero(b_or != b_g)[0]
+    if moved.size == 0:
+        return 0
+    if np.any(np.abs(b_or[moved] - b_g[moved]) != 1):
+        return None
+    # the oracle's score at the first rank of each bin j = 1..K-1
+    order = np.lexsort((np.arange(N), v_or))
+    edge_val = {}
+    for j in range(1, K):
+        r = -(-j * N // K)              # ceil(j N / K): first rank of bin j
+        if r < N:
+            edge_val[j] = v_or[order[r]]
+    for t in moved:
+        j = max(b_or[t], b_g[t])        # the edge between bins j-1 and j
+        e = edge_val.get(j)
+        if e is None or abs(v_or[t] - e) > REL * abs(e):
+            return None
+    return int(moved.size)
+
+
 def check_layer(tag, K, V, L, W, spans, F, B, op: O.Params, G, gpu: dict,
                 orc: dict, report: dict):
     """Compare one layer.  K, V: storage arrays [G, L, d]; gpu: this layer's
@@ -101,8 +147,21 @@ def check_layer(tag, K, V, L, W, spans, F, B, op: O.Params, G, gpu: dict,
     assert abs(f["h_hat"] - h_stage) <= 1e-5 and abs(f["T"] - T_stage) <= 1e-5, f"{tag}: H/T stage"
 
     # ---- online statistics, end to end
-    assert np.max(np.abs(f["mi"] - orc["mi"])) <= 2e-3, f"{tag}: MI e2e {f['mi']} vs {orc['mi']}"
-    assert np.max(np.abs(f["mi_bar"] - orc["mi_bar"])) <= 2e-3, f"{tag}: MI_bar e2e"
+    mi_tol = np.full(G, 2e-3)
+    n_moved = 0
+    for g in range(G):
+        moved = near_tie_bin_moves(orc["S"][g, vis], S_g[g, vis], op.n_bins)
+        if moved is None:
+            raise AssertionError(f"{tag}: group {g} rank bins differ off a near tie")
+        if moved:
+            n_moved += moved
+            mi_tol[g] += abs(mi_stage[g] - orc["mi"][g])
+    assert np.all(np.abs(f["mi"] - orc["mi"]) <= mi_tol), f"{tag}: MI e2e {f['mi']} vs {orc['mi']}"
+    mibar_tol = 2e-3 + (1.0 - op.rho_mi) * (mi_tol - 2e-3)
+    assert np.all(np.abs(f["mi_bar"] - orc["mi_bar"]) <= mibar_tol), f"{tag}: MI_bar e2e"
+    mb_delta = float(np.max(np.abs(f["mi_bar"].astype(np.float64) - orc["mi_bar"])))
+    mb_gap = float(np.max(orc["mi_bar"]) - np.min(orc["mi_bar"]))
+    prior_ill = G > 1 and mb_gap <= 100.0 * mb_delta + 1e-7
     assert abs(f["lam"] - orc["lam_eff"]) <= 1e-6, f"{tag}: lambda"
     assert np.max(np.abs(f["phi"] - orc["phi"])) <= 1e-4, f"{tag}: phi {f['phi']} vs {orc['phi']}"
     assert abs(f["h_hat"] - orc["h_hat"]) <= 1e-4 and abs(f["T"] - orc["T"]) <= 1e-4, f"{tag}: H/T"
@@ -119,10 +178,16 @@ def check_layer(tag, K, V, L, W, spans, F, B, op: O.Params, G, gpu: dict,
     # above (both choices valid) the oracle's fusion is evaluated with the
     # GPU's choice, from the oracle's own w, phi, lambda and T
     s_or = orc["s"]
+    if prior_ill and orc["lam_eff"] > 0:
+        # w is not fixed by the tolerance: the oracle's fusion with the GPU's w
+        w_g = f["w"].astype(np.float64)
+        beta_i = (1.0 - orc["lam_eff"]) + orc["lam_eff"] * G * w_g[orc["gstar"]]
+        s_or = O.final_score(orc["sbar"], beta_i, orc["D"], orc["T"])[1]
     if mism.size:
         s_or = s_or.copy()
         gm = gst_g[mism]
-        beta_m = (1.0 - orc["lam_eff"]) + orc["lam_eff"] * G * orc["w"][gm]
+        w_m = f["w"].astype(np.float64) if prior_ill else orc["w"]
+        beta_m = (1.0 - orc["lam_eff"]) + orc["lam_eff"] * G * w_m[gm]
         D_m = O.temporal_discount(is_vis[mism], frame[mism], F, orc["phi"][gm],
                                   op.delta, op.d_min, op.tem_decay)
         s_or[mism] = O.final_score(orc["sbar"][mism], beta_m, D_m, orc["T"])[1]
@@ -147,6 +212,8 @@ def check_layer(tag, K, V, L, W, spans, F, B, op: O.Params, G, gpu: dict,
     if np.array_equal(idx_g, orc["I"]):
         assert np.array_equal(gpu["k_out"], orc["K_out"])
 
+    report.setdefault("bin_moves", []).append(n_moved)
+    report.setdefault("prior_ill", []).append(int(prior_ill))
     report.setdefault("S", []).append(r_S)
     report.setdefault("s", []).append(r_s)
     report.setdefault("idx_band", []).append(ndiff)

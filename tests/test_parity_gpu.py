@@ -140,9 +140,10 @@ def test_config3_layer_groups_on_two_streams():
 
 
 def test_config4_budget_sweep_sampled_layers():
-    """15 steps, three budgets per step; the oracle follows layers 0 and 13
-    through the whole trajectory (their state depends on every step)."""
-    run_trajectory(4, layers=[0, 13])
+    """15 steps, three budgets per step; the oracle follows layers 0, 9, 18
+    and 27 through the whole trajectory (their state depends on every
+    step)."""
+    run_trajectory(4, layers=[0, 9, 18, 27])
 
 
 def oracle_state_from_gpu(state_bytes_np, layer, G, frame_cap):
@@ -162,8 +163,11 @@ def oracle_state_from_gpu(state_bytes_np, layer, G, frame_cap):
 def test_config5_long_trajectory_sampled_steps():
     """The 30-step 2560x1440 trajectory (W = 64: 448 window rows per group,
     up to 140K past tokens, keys beyond every LDS cache) for layers 0 and 27
-    on the GPU.  At steps 1, 2, 16 and 30 the oracle runs that step from the
-    GPU's own state after the previous step, and every output is compared."""
+    on the GPU.  Layer 0: the oracle carries its own state through all 30
+    steps; at steps 1, 2, 16 and 30 every output is compared, and so are the
+    stability means m_g and MI_bar the GPU state holds afterwards (the
+    stability row of 4641 tokens, sec. 3.5).  Layer 27: at the same steps the
+    oracle runs that step from the GPU's own state after the previous one."""
     spec = WL.SPECS[5]
     p = params_for(5)
     op = oracle_params(p)
@@ -172,6 +176,7 @@ def test_config5_long_trajectory_sampled_steps():
     frame_cap = spec.n_frame
     case = ArrayCase(spec.H, spec.G, spec.d, spec.W, len(layers), spec.L(spec.steps),
                      spec.dtype, p, frame_cap)
+    own = O.LayerState(spec.G)          # layer 0's oracle state, every step
     report = {}
     for step in range(1, spec.steps + 1):
         L, spans, B = spec.L(step), spec.spans(step), spec.budgets(step)[0]
@@ -180,22 +185,34 @@ def test_config5_long_trajectory_sampled_steps():
         Vs = np.stack([c[1] for c in caches])
         Qs = np.stack([host.tr.window_q(layer, step) for layer in layers])
         check = step in (1, 2, 16, 30)
-        if check:
-            prev = case.state.cpu().numpy()
+        prev = case.state.cpu().numpy()
         say(f"cfg5 step {step}: L={L} B={B}{' (checked)' if check else ''}")
         gpu = case.run(Qs, Ks, Vs, L, spans, step, B)
+        out0, own = O.compress_layer(WL.to_float64(Qs[0], spec.dtype),
+                                     WL.to_float64(Ks[0], spec.dtype), None, L, spec.W,
+                                     spans, step, B, op, own, copy_rows=(Ks[0], Vs[0]))
         if not check:
             continue
+        after = case.state.cpu().numpy()
         for i, layer in enumerate(layers):
-            st = oracle_state_from_gpu(prev, i, spec.G, frame_cap)
-            out, _ = O.compress_layer(WL.to_float64(Qs[i], spec.dtype),
-                                      WL.to_float64(Ks[i], spec.dtype), None, L, spec.W,
-                                      spans, step, B, op, st, copy_rows=(Ks[i], Vs[i]))
+            if i == 0:
+                out = out0
+            else:
+                st = oracle_state_from_gpu(prev, i, spec.G, frame_cap)
+                out, _ = O.compress_layer(WL.to_float64(Qs[i], spec.dtype),
+                                          WL.to_float64(Ks[i], spec.dtype), None, L, spec.W,
+                                          spans, step, B, op, st, copy_rows=(Ks[i], Vs[i]))
             g = {k: v[i] for k, v in gpu.items()}
             check_layer(f"cfg5 step{step} L{layer}", Ks[i], Vs[i], L, spec.W, spans, step,
                         B, op, spec.G, g, out, report)
+        gst = oracle_state_from_gpu(after, 0, spec.G, frame_cap)
+        assert gst.n == own.n == step
+        assert gst.m.shape == own.m.shape == (spec.G, spec.n_frame)
+        np.testing.assert_allclose(gst.m, own.m, rtol=1e-3, atol=1e-9,
+                                   err_msg=f"cfg5 step{step}: stability means m_g")
+        assert np.max(np.abs(gst.mi_bar - own.mi_bar)) <= 2e-3, f"cfg5 step{step}: MI_bar state"
     say(f"cfg5 done: max S rel {max(report['S']):.2e}, idx band tokens "
-        f"{sum(report['idx_band'])}")
+        f"{sum(report['idx_band'])}, rank-bin near-tie moves {sum(report['bin_moves'])}")
 
 
 def test_determinism_bitwise():
@@ -438,13 +455,13 @@ def test_rank_bins_and_grid_extremes(n_bins, grid, rows, cols):
     with 2,400 visual tokens (keys in LDS) and 24,000 (keys read from
     memory): K = 33 is the largest that takes the fused pass, K = 64 with
     M = 16 fills the whole joint histogram.  MI and w are compared stage-wise
-    and end to end; lambda = 0 keeps beta = 1, because on random inputs the
-    groups' MIs can lie within rounding of each other (1.5e-4 apart at
-    K = 33 on 24,000 tokens), where the min-max prior may rank them either
-    way and the fused score then differs by the prior's full weight."""
+    and end to end, with the prior active (lambda = 0.5 from the first
+    step).  On random inputs the two groups' MIs can lie within rounding of
+    each other (1.5e-4 apart at K = 33 on 24,000 tokens), where min-max
+    ranks them either way: the near-tie rule of tests/parity.py then takes
+    the oracle's fusion with the GPU's w."""
     p = params_for(2, prior_active=True)
     p.n_bins, p.grid = n_bins, grid
-    p.lam = 0.0
     H, G, d, W = 8, 2, 64, 8
     L = rows * cols + 200
     spans = [(100, rows, cols, 1)]
