@@ -64,6 +64,9 @@ def parse():
                     help="temporal discount variant of the decay ablation (exp is the paper's)")
     ap.add_argument("--aeb", choices=["entropy", "confidence"], default="entropy",
                     help="AEB temperature variant of the ablation (entropy is the paper's)")
+    ap.add_argument("--budget-pct", type=int, default=None,
+                    help="run the workload at this one of its budget percentages "
+                         "(default: the first)")
     ap.add_argument("--per-head", action="store_true",
                     help="a scoring subspace per query head (the MHA-head granularity "
                          "on the GQA model) instead of one per KV group")
@@ -265,7 +268,7 @@ def main():
     from paper_2606_01790_amd import workload as WL
 
     assert torch.cuda.is_available(), "no GPU visible"
-    spec = WL.SPECS[args.config]
+    spec = pick_budget(WL.SPECS[args.config], args.budget_pct)
     params = sk.params_default()
     if args.config >= 3:
         params.t_min, params.t_max = 0.95, 1.05
@@ -273,7 +276,9 @@ def main():
     log(f"workload {spec.name}: building resident inputs")
     n_states = args.warmup + 3
     wl = Workload(spec, params, n_states, per_head=args.per_head)
-    workload = (spec.name + ("-per-head" if args.per_head else "")
+    sweep = len(WL.SPECS[args.config].pcts) > 1
+    workload = (spec.name + (f"-at-{spec.pcts[0]}pct" if sweep else "")
+                + ("-per-head" if args.per_head else "")
                 + ("" if args.tem_decay == "exp" else f"-tem-{args.tem_decay}")
                 + ("" if args.aeb == "entropy" else f"-aeb-{args.aeb}"))
     layer_tokens = spec.n_layers * sum(spec.n_vis(s) for s in range(1, spec.steps + 1))
@@ -335,7 +340,10 @@ def main():
                          "kernel": f"starkv_{dom}",
                          "avg_launch_us": round(avg_s * 1e6, 2),
                          "alg_bytes_per_launch": int(avg_b),
-                         "alg_flops_per_launch": int(avg_f)})
+                         "alg_flops_per_launch": int(avg_f),
+                         # the contraction's rate against the dense MFMA peak of
+                         # its input type, whichever roof binds
+                         "mfma_frac": round(avg_f / avg_s / 1e12 / MFMA_PEAK_TFLOPS[spec.dtype], 4)})
         per_call_us = {n: round(per[n]["time"] / per[n]["launches"] * 1e6, 2) for n in per}
 
     copy_gbs = measure_copy_bandwidth(torch)
@@ -397,7 +405,7 @@ def decode_bench(args):
     from paper_2606_01790_amd import workload as WL
     from paper_2606_01790_amd.pipeline import TrajectoryRunner
 
-    spec = WL.SPECS[args.config]
+    spec = pick_budget(WL.SPECS[args.config], args.budget_pct)
     params = sk.params_default()
     if args.config >= 3:
         params.t_min, params.t_max = 0.95, 1.05
@@ -600,6 +608,17 @@ def blas_threads():
         return max(blas) if blas else 1
     except Exception:
         return 1
+
+
+def pick_budget(spec, pct):
+    """The workload at one of its budget percentages (the first by default);
+    the inputs do not depend on the budget."""
+    import dataclasses
+    if pct is None:
+        pct = spec.pcts[0]
+    if pct not in spec.pcts:
+        sys.exit(f"bench: {spec.name} runs at budgets {list(spec.pcts)} percent, not {pct}")
+    return dataclasses.replace(spec, pcts=(pct,))
 
 
 def cpu_baseline(spec, params, seconds, per_head=False, tem_decay="exp", aeb="entropy"):
