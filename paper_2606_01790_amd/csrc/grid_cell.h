@@ -15,13 +15,25 @@ namespace starkv {
 
 // floor(x * M / n) without an integer division, for 0 <= x < n,
 // 1 <= M <= 16 and n < 2^27 (so x * M < 2^31).  The quotient is below M,
-// so the float estimate is within one of it and one correction step makes
-// it exact.
+// so a float estimate m_over_n of M / n good to a few ulps puts x *
+// m_over_n within one of it, and one correction step makes it exact.
 STARKV_HD inline int scaled_index(int x, int M, int n, float m_over_n) {
   int q = (int)((float)x * m_over_n);
   const int xm = x * M;
   if (q * n > xm) --q;
   else if ((q + 1) * n <= xm) ++q;
+  return q;
+}
+
+// floor(p / n) for 0 <= p < kSmallQuot and n >= 1, from rn, the reciprocal
+// of n to within one ulp: there the estimate p * rn is within one of the
+// quotient (n = 1 and 2 have exact reciprocals; for n >= 3 the error is at
+// most p / n * 2^-22 < 1/3), and one correction step makes it exact.
+constexpr int kSmallQuot = 1 << 22;
+STARKV_HD inline int small_quot(int p, int n, float rn) {
+  int q = (int)((float)p * rn);
+  if (q * n > p) --q;
+  else if ((q + 1) * n <= p) ++q;
   return q;
 }
 

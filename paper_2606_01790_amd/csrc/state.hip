@@ -76,6 +76,7 @@ constexpr int kThreads = 1024;
 constexpr int kWaves = kThreads / 64;
 constexpr int kBatch = 8;                 // loads in flight per thread
 constexpr int kKeyBatch = 8;              // keys per thread per rank-binning step
+constexpr int kLoadBatch = 16;            // loads in flight in the first pass over S
 constexpr int kHistInts = 16384;          // 64 KiB: digit or joint histograms
 constexpr int kKeyCache = 20 * 1024;      // visual keys kept in LDS
 constexpr int kCand = 2048;               // keys in the edges' first-digit buckets
@@ -338,8 +339,11 @@ __device__ __forceinline__ void stats_body(const StatsArgs& a) {
     };
     // Grid cell of visual index i.  A pass visits a thread's indices in
     // steps of kThreads, so (row, col) step inside a span and are recomputed
-    // from the index (a float-estimated division) only when it enters
-    // another span.
+    // from the index only when it enters another span.  There the position
+    // in the span is below kThreads (the previous index lay before the
+    // span), so the row and every per-span constant come from reciprocal
+    // estimates with one exact correction step; only a first index deep
+    // inside a span takes the integer division.
     int q_s = 0, q_r = 0, q_c = 0, q_end = 0, q_next = -1, q_rows = 1, q_cols = 1,
         q_dq = 0, q_dr = 0;
     float q_fr = 0.f, q_fc = 0.f;
@@ -349,11 +353,19 @@ __device__ __forceinline__ void stats_body(const StatsArgs& a) {
         q_rows = sp_rows[q_s];
         q_cols = sp_cols[q_s];
         q_end = sp_off[q_s + 1];
-        span_row_col(i - sp_off[q_s], q_cols, &q_r, &q_c);
-        q_dq = kThreads / q_cols;
+        const float rc = __builtin_amdgcn_rcpf((float)q_cols);
+        const int p = i - sp_off[q_s];
+        if (p < kSmallQuot) {
+          q_r = small_quot(p, q_cols, rc);
+          q_c = p - q_r * q_cols;
+        } else {
+          span_row_col(p, q_cols, &q_r, &q_c);
+        }
+        q_dq = small_quot(kThreads, q_cols, rc);
         q_dr = kThreads - q_dq * q_cols;
-        q_fr = (float)M / (float)q_rows;
-        q_fc = (float)M / (float)q_cols;
+        // estimates of M / rows and M / cols: grid_cell corrects them
+        q_fr = (float)M * __builtin_amdgcn_rcpf((float)q_rows);
+        q_fc = (float)M * rc;
       } else {
         q_c += q_dr;
         q_r += q_dq;
@@ -365,19 +377,26 @@ __device__ __forceinline__ void stats_body(const StatsArgs& a) {
     auto cell_reset = [&]() { q_s = 0; q_next = -1; };
 
     // ---- visual keys (LDS when they fit), min and max
+    // (the first read of S: kLoadBatch loads in flight, so the five-frame
+    // sizes take one round trip)
     uint32_t lo = 0xFFFFFFFFu, hi = 0u;
     {
       fetch_reset();
-      for (int i0 = tid; i0 < N; i0 += kKeyBatch * kThreads) {
-        uint32_t kv[kKeyBatch];
-        fetch(i0, kv);
+      for (int i0 = tid; i0 < N; i0 += kLoadBatch * kThreads) {
+        float v[kLoadBatch];
 #pragma unroll
-        for (int u = 0; u < kKeyBatch; ++u) {
+        for (int u = 0; u < kLoadBatch; ++u) {
+          const int i = i0 + u * kThreads;
+          v[u] = i < N ? Sg[token_of(i)] : 0.f;
+        }
+#pragma unroll
+        for (int u = 0; u < kLoadBatch; ++u) {
           const int i = i0 + u * kThreads;
           if (i < N) {
-            if (cached) kc[i] = kv[u];
-            lo = min(lo, kv[u]);
-            hi = max(hi, kv[u]);
+            const uint32_t key = fkey(v[u]);
+            if (cached) kc[i] = key;
+            lo = min(lo, key);
+            hi = max(hi, key);
           }
         }
       }
@@ -593,18 +612,28 @@ __device__ __forceinline__ void stats_body(const StatsArgs& a) {
 #pragma unroll
           for (int j = 0; j < 8; ++j)
             eb[j] = j < n_t ? ((t_key[j] >> shift) & (uint32_t)(nb - 1)) : 0xFFFFFFFFu;
+          // per first-digit bucket, in the digit histogram's place (read
+          // by the scan above, not needed again before the next digit): the
+          // number of edges in lower buckets, i.e. the bin of a key outside
+          // the edges' buckets, with bit 8 set for an edge's own bucket
+          // (bins < 64)
+          int* const d_lut = hist;
+          for (int dd = tid; dd < nb; dd += kThreads)
+            d_lut[dd] = lower_edges((uint32_t)dd) |
+                        (int)(((bucket_bits[dd >> 5] >> (dd & 31)) & 1u) << 8);
           __syncthreads();
           fetch_reset();
           auto fuse_key = [&](int i, uint32_t key) {
             const uint32_t d = (key >> shift) & (uint32_t)(nb - 1);
             const int cell = cell_at(i);
-            if ((bucket_bits[d >> 5] >> (d & 31)) & 1u) {
+            const int lut = d_lut[d];
+            if (lut & 0x100) {
               const int sg = seg_of_bucket(d);
               const int pos = seg_off[sg] + atomicAdd(&seg_cur[sg], 1);
               ck[pos] = key;
               cv[pos] = ((uint32_t)cell << 24) | (uint32_t)i;
             } else {
-              atomicAdd(&jh[lower_edges(d) * ncell + cell], 1);
+              atomicAdd(&jh[lut * ncell + cell], 1);
             }
           };
           cell_reset();

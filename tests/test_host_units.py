@@ -63,17 +63,32 @@ def test_grid_cells_exact_at_large_positions(tmp_path):
     rnd = random.Random(5)
     cases = []
     big = 1 << 26                                   # largest span the boundary accepts
+    small = 1 << 22                                 # the reciprocal-estimate path's limit
     for rows, cols in [(big, 1), (big // 2, 2), (big // 3, 3), (1, big), (8191, 8192),
-                       (4096 * 4, 4096), (39, 69), (51, 91), (4000, 4000), (3, big // 3)]:
+                       (4096 * 4, 4096), (39, 69), (51, 91), (26, 46), (4000, 4000),
+                       (3, big // 3), (7, 3), (1, 1), (1025, 1023), (2, 1024)]:
         n = rows * cols
         for M in (1, 7, 8, 16):
-            pts = {0, n - 1, n // 2, n // 3, min(n - 1, 33554434), min(n - 1, (1 << 25) - 1)}
+            pts = {0, n - 1, n // 2, n // 3, min(n - 1, 33554434), min(n - 1, (1 << 25) - 1),
+                   min(n - 1, small - 1), min(n - 1, small), min(n - 1, 1023)}
             pts |= {rnd.randrange(n) for _ in range(40)}
+            pts |= {rnd.randrange(min(n, 1024)) for _ in range(20)}
             cases += [(p, rows, cols, M) for p in sorted(pts)]
     got = _cells(exe, cases)
     assert len(got) == len(cases)
-    for (p, rows, cols, M), (r, c, cell) in zip(cases, got):
+    for (p, rows, cols, M), (r, c, cell, ok) in zip(cases, got):
         assert (r, c) == divmod(p, cols), (p, rows, cols)
         want = (r * M // rows) * M + (c * M // cols)
         assert cell == want, (p, rows, cols, M, cell, want)
         assert 0 <= cell < M * M
+        # the kernel's span-entry path: reciprocal estimates one ulp off
+        assert ok == 1, (p, rows, cols, M)
+
+
+def test_small_quotient_exact_near_every_multiple(tmp_path):
+    exe = _build(tmp_path, "grid_cell_driver", [os.path.join(HOST, "grid_cell_driver.cpp")],
+                 sanitize=False)
+    r = subprocess.run([exe, "quot"], capture_output=True, text=True, timeout=300)
+    assert r.returncode == 0, r.stderr
+    bad, checked = map(int, r.stdout.split())
+    assert checked > 10**6 and bad == 0, (bad, checked)
