@@ -2,9 +2,11 @@
 // sec. 3.7 selection).  One 1024-thread workgroup per layer:
 //   1. s_t = max(sbar_t * beta_t * D_t, 0)^(1/T) for every past token
 //      (D_t with the configured decay: exponential, linear or gamma),
-//      written out and kept as a descending-order key in LDS (the span of a
-//      token comes from an LDS copy of the span table, walked by a cursor
-//      since each thread's tokens ascend);
+//      written out and kept as a descending-order key in LDS.  beta_t and
+//      D_t depend on the token only through g*_t and its span, so both come
+//      from tables filled once per block (per group; per group and span);
+//      the span of a token comes from an LDS copy of the span table, walked
+//      by a cursor since each thread's tokens ascend;
 //   2. MSB-first radix select of the B-th key in the order (s descending,
 //      token index ascending): the bits every key shares are skipped, the
 //      first digit is 12 bits wide (one histogram, block-wide scan); the keys
@@ -26,6 +28,7 @@ namespace {
 constexpr int kThreads = 1024;
 constexpr int kWaves = kThreads / 64;
 constexpr int kBatch = 8;              // loads in flight per thread
+constexpr int kScoreBatch = 16;        // tokens per thread per step of the fused score
 constexpr int kLdsKeys = 28 * 1024;   // keys cached in LDS (112 KiB)
 constexpr int kCand = 2048;           // keys of the cut's first-digit bucket
 constexpr int kDirect = 256;          // candidates ranked directly, no more digits
@@ -50,11 +53,12 @@ __global__ __launch_bounds__(kThreads) void select_kernel(SelArgs a) {
   __shared__ int hist[4096];              // first digit; later per-wave digits
   __shared__ __align__(16) uint32_t cand[kCand];
   __shared__ int sp_start[STARKV_MAX_SPANS], sp_end[STARKV_MAX_SPANS];
-  __shared__ float sp_dist[STARKV_MAX_SPANS];
-  __shared__ float sp_ldist[STARKV_MAX_SPANS];   // log2(1 + distance), gamma decay
   __shared__ int sh_cnt[kWaves];
   __shared__ int n_cand;
-  __shared__ float w_s[STARKV_MAX_GROUPS], phi_s[STARKV_MAX_GROUPS];
+  __shared__ float beta_s[STARKV_MAX_GROUPS];
+  // D of a visual token depends only on its group g* and its span (the
+  // frame distance): one entry per (group, span), row-major by group
+  __shared__ float d_tab[STARKV_MAX_GROUPS * STARKV_MAX_SPANS];
   __shared__ uint32_t red_lo[kWaves], red_hi[kWaves];
   __shared__ uint32_t cut_key;
   __shared__ int cut_rank, cut_eq;
@@ -66,21 +70,28 @@ __global__ __launch_bounds__(kThreads) void select_kernel(SelArgs a) {
   const float* sb = a.sbar + (size_t)layer * a.Lp;
   const uint8_t* gs = a.gstar + (size_t)layer * a.Lp;
   float* s_out = a.s + (size_t)layer * a.Lp;
-  if (tid < a.G) {
-    w_s[tid] = scal[STARKV_SCAL_W(a.G) + tid];
-    phi_s[tid] = scal[STARKV_SCAL_PHI(a.G) + tid];
-  }
-  if (tid < a.n_spans) {
-    sp_start[tid] = a.start[tid];
-    sp_end[tid] = a.end[tid];
-    sp_dist[tid] = (float)(a.frame - a.sframe[tid]);
-    sp_ldist[tid] = __log2f(1.0f + sp_dist[tid]);
-  }
-  __syncthreads();
   const float lam = scal[STARKV_SCAL_LAMBDA(a.G)];
   const float T = scal[STARKV_SCAL_T(a.G)];
   const float inv_t = 1.0f / T;
   const float gl = (float)a.G * lam;
+  // the tables, straight from the layer's scalars (one barrier)
+  if (tid < a.G) beta_s[tid] = (1.0f - lam) + gl * scal[STARKV_SCAL_W(a.G) + tid];
+  if (tid < a.n_spans) {
+    sp_start[tid] = a.start[tid];
+    sp_end[tid] = a.end[tid];
+  }
+  for (int e = tid; e < a.G * a.n_spans; e += kThreads) {
+    const int g = e / a.n_spans, sp = e - g * a.n_spans;
+    const float phi = scal[STARKV_SCAL_PHI(a.G) + g];
+    const float dist = (float)(a.frame - a.sframe[sp]);
+    const float dp = a.delta * phi;
+    float f;
+    if (a.tem == STARKV_TEM_EXP) f = __expf(-a.delta * dist * phi);
+    else if (a.tem == STARKV_TEM_LINEAR) f = fmaxf(0.0f, 1.0f - dp * dist);
+    else f = exp2f(-dp * __log2f(1.0f + dist));   // gamma: (1 + distance)^(-delta phi)
+    d_tab[e] = a.d_min + (1.0f - a.d_min) * f;
+  }
+  __syncthreads();
 
   // Keys of tokens t0 + u * step, u < kBatch, at or past the LDS cache
   // (0xFFFFFFFF past Lp), read back from s with kBatch loads in flight.
@@ -99,31 +110,24 @@ __global__ __launch_bounds__(kThreads) void select_kernel(SelArgs a) {
   // ---- 1. fused score; keys order tokens by descending s
   uint32_t lo = 0xFFFFFFFFu, hi = 0u;
   int cur = 0;   // first span that does not end at or before this thread's token
-  for (int t0 = tid; t0 < a.Lp; t0 += kBatch * kThreads) {
-    float sbv[kBatch];
-    int gv[kBatch];
+  for (int t0 = tid; t0 < a.Lp; t0 += kScoreBatch * kThreads) {
+    float sbv[kScoreBatch];
+    int gv[kScoreBatch];
 #pragma unroll
-    for (int u = 0; u < kBatch; ++u) {   // kBatch loads in flight
+    for (int u = 0; u < kScoreBatch; ++u) {   // 2 * kScoreBatch loads in flight
       const int t = t0 + u * kThreads;
       sbv[u] = t < a.Lp ? sb[t] : 0.f;
       gv[u] = t < a.Lp ? (int)gs[t] : 0;
     }
 #pragma unroll
-    for (int u = 0; u < kBatch; ++u) {
+    for (int u = 0; u < kScoreBatch; ++u) {
       const int t = t0 + u * kThreads;
       if (t < a.Lp) {
         const int g = min(gv[u], a.G - 1);
-        const float beta = (1.0f - lam) + gl * w_s[g];
+        const float beta = beta_s[g];
         float D = 1.0f;
         while (cur < a.n_spans && sp_end[cur] <= t) ++cur;
-        if (cur < a.n_spans && sp_start[cur] <= t) {
-          const float dp = a.delta * phi_s[g];
-          float f;
-          if (a.tem == STARKV_TEM_EXP) f = __expf(-a.delta * sp_dist[cur] * phi_s[g]);
-          else if (a.tem == STARKV_TEM_LINEAR) f = fmaxf(0.0f, 1.0f - dp * sp_dist[cur]);
-          else f = exp2f(-dp * sp_ldist[cur]);
-          D = a.d_min + (1.0f - a.d_min) * f;
-        }
+        if (cur < a.n_spans && sp_start[cur] <= t) D = d_tab[g * a.n_spans + cur];
         const float sf = fmaxf(sbv[u] * beta * D, 0.0f);
         const float sv = (inv_t == 1.0f || sf == 0.0f) ? sf : exp2f(inv_t * __log2f(sf));
         s_out[t] = sv;
