@@ -320,6 +320,21 @@ def test_token_tail_sweep(Lp):
              seed=Lp)
 
 
+@pytest.mark.parametrize("k,Lp", [(1, 1), (3, 5), (5, 255), (7, 257), (9, 1025), (63, 700)])
+def test_pool_width_sweep(k, Lp):
+    """AvgPool1D widths from 1 to 63 (the widest accepted), with token counts
+    on both sides of the pooling kernel's 256-token tiles and a pool wider
+    than a short row (zero padding on both sides, halos crossing tiles)."""
+    p = params_for(2)
+    p.pool_kernel = k
+    W = 8
+    L = Lp + W
+    rows, cols = min(Lp, 10), max(min(Lp // 10, 12), 1)
+    spans = [(0, rows, cols, 1)] if rows * cols <= Lp else []
+    run_case(f"pool k={k} Lp={Lp}", 8, 2, 64, W, L, spans, 1, max(Lp // 5, 1), "bf16", p,
+             seed=40 + k)
+
+
 def test_budget_extremes():
     p = params_for(2)
     spans = [(0, 10, 20, 1)]
