@@ -1,7 +1,7 @@
 // bf16 instantiations of the scoring passes (v_mfma_f32_32x32x16_bf16).
-// With d = 128 and one subspace per KV group, pass 2 runs on the persistent
-// slab kernel of score_slab.h; other shapes use the tile kernels of both
-// passes.
+// With d = 128 and one subspace per KV group, or per-head subspaces whose
+// heads are whole 32-row blocks, pass 2 runs on the persistent slab kernel
+// of score_slab.h; other shapes use the tile kernels of both passes.
 #include <algorithm>
 
 #include "score_slab.h"
@@ -21,7 +21,10 @@ int slab_passes(const ScoreArgs& a, int n_layers, int n_cu, hipStream_t st) {
   // one block per CU (the kernel holds two 256-VGPR waves per SIMD), never
   // more blocks than slabs
   const int nb = (int)std::min<long>(n_cu, (long)sg.S * sg.nlg);
-  score_pass2_slab<NRB><<<nb, 512, SlabLds<NRB>::kBytes, st>>>(a, sg);
+  if (a.n_out > 1)
+    score_pass2_slab<NRB, true><<<nb, 512, SlabLds<NRB>::kBytes, st>>>(a, sg);
+  else
+    score_pass2_slab<NRB, false><<<nb, 512, SlabLds<NRB>::kBytes, st>>>(a, sg);
   return (int)hipGetLastError();
 }
 
@@ -40,7 +43,7 @@ int run_pass2_slab(const ScoreArgs& a, int n_layers, int n_cu, hipStream_t st) {
 }
 
 int run_score_bf16(const ScoreArgs& a, int d, int n_layers, hipStream_t st) {
-  if (d == 128 && a.n_out == 1 && a.Rpad / 32 <= kSlabMaxNrb) {
+  if (d == 128 && a.Rpad / 32 <= kSlabMaxNrb && (a.n_out == 1 || a.n_part == 1)) {
     int dev = 0, n_cu = 0;
     if (hipGetDevice(&dev) != hipSuccess ||
         hipDeviceGetAttribute(&n_cu, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||

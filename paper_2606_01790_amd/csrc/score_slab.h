@@ -1,7 +1,10 @@
 // Pass 2 of the window scoring (sec. 3.3, Eq. A_raw) for bf16 keys with
-// d = 128 and one scoring subspace per KV group: for every past token t of
-// a (layer, group), sum_r 2^(y_rt - c_r) over the group's R window rows,
-// with y = q.k * log2(e)/sqrt(d) and c_r the row's log2-sum-exp from pass 1.
+// d = 128: for every past token t of a (layer, group), sum_r 2^(y_rt - c_r)
+// over the group's R window rows, with y = q.k * log2(e)/sqrt(d) and c_r the
+// row's log2-sum-exp from pass 1.  With one scoring subspace per KV group
+// the sum runs over all R rows; with per-head subspaces (PH), when each
+// head's W rows are whole 32-row blocks, over each head's own rows, one
+// output per head.
 //
 // Persistent design: one 512-thread block per CU walks a contiguous range
 // of the flattened (layer-group, 64-token slab) space.  For each group
@@ -42,7 +45,7 @@ __device__ inline int slab_block() {
   return xcd < rem ? xcd * (per + 1) + local : rem * (per + 1) + (xcd - rem) * per + local;
 }
 
-template <int NRB>
+template <int NRB, bool PH>
 __global__ __launch_bounds__(512) void score_pass2_slab(ScoreArgs a, SlabGrid sg) {
   using T = __bf16;
   using M = Mfma<T>;
@@ -67,7 +70,8 @@ __global__ __launch_bounds__(512) void score_pass2_slab(ScoreArgs a, SlabGrid sg
     const int s1 = (int)min((long)sg.S, s0 + (hi - x));
     const int layer = lg / a.G, g = lg % a.G;
     const T* kg = group_k<T>(a, layer, g);
-    float* srow = a.sraw + (size_t)lg * a.Lp;
+    // the group's first output row: its only one, or its first head's
+    float* srow = a.sraw + (size_t)lg * (PH ? a.n_out : 1) * a.Lp;
 
     // the group's window rows (rows R..NRB*32 zero), in batches of at most
     // seven 16-byte vectors per thread, each batch's loads issued before
@@ -176,18 +180,33 @@ __global__ __launch_bounds__(512) void score_pass2_slab(ScoreArgs a, SlabGrid sg
           asm volatile("" : "+v"(s[cb][0]));
           asm volatile("" : "+v"(s[cb][1]));
         }
+        if (PH && (rb + 1) % a.upo == 0) {
+          // the last row block of head rb / upo: its output, then a fresh sum
+          float* hrow = srow + (size_t)(rb / a.upo) * a.Lp;
+#pragma unroll
+          for (int cb = 0; cb < TB; ++cb) {
+            const float sc = s[cb][0] + s[cb][1];
+            const float v = sc + other_half(sc, half);
+            const int tok = slab * SLAB + cb * 32 + l32;
+            if ((cb & 1) == half && tok < a.Lp) hrow[tok] = v;
+            s[cb][0] = 0.f;
+            s[cb][1] = 0.f;
+          }
+        }
         __builtin_amdgcn_sched_barrier(0);
       }
       const int t0 = slab * SLAB;
       if (slab + NW < s1) load_slab(slab + NW);
       // lanes l and l ^ 32 hold the same token's two row halves; half h
       // stores token block h
+      if (!PH) {
 #pragma unroll
-      for (int cb = 0; cb < TB; ++cb) {
-        const float sc = s[cb][0] + s[cb][1];
-        const float v = sc + other_half(sc, half);
-        const int tok = t0 + cb * 32 + l32;
-        if ((cb & 1) == half && tok < a.Lp) srow[tok] = v;
+        for (int cb = 0; cb < TB; ++cb) {
+          const float sc = s[cb][0] + s[cb][1];
+          const float v = sc + other_half(sc, half);
+          const int tok = t0 + cb * 32 + l32;
+          if ((cb & 1) == half && tok < a.Lp) srow[tok] = v;
+        }
       }
     }
     x += s1 - s0;
@@ -198,7 +217,9 @@ __global__ __launch_bounds__(512) void score_pass2_slab(ScoreArgs a, SlabGrid sg
 
 }  // namespace
 
-// Pass 2 on the slab kernel: R = NRB*32-padded rows, NRB <= kSlabMaxNrb.
+// Pass 2 on the slab kernel: R = NRB*32-padded rows, NRB <= kSlabMaxNrb;
+// per-head subspaces need each head's rows to be whole row blocks (n_part
+// 1, upo row blocks per head).
 constexpr int kSlabMaxNrb = 14;
 int run_pass2_slab(const ScoreArgs& a, int n_layers, int n_cu, hipStream_t st);
 
