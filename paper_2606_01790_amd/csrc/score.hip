@@ -12,34 +12,45 @@ namespace {
 // S[g,t] = (1/(k*hps)) sum_{|j|<=k/2} S_raw[g,t+j] (zero outside [0,L_p))
 // for each of the G scoring subspaces (hps heads each), sbar = mean over
 // subspaces, g* = first argmax.  The pooled sum adds the k window values in
-// token order.
+// token order; the mean and the argmax take the subspaces in order.
+constexpr int kAggChunk = 8;   // subspaces per LDS tile
+
 __global__ __launch_bounds__(256) void score_aggregate(const float* sraw, float* S,
                                                        float* sbar, uint8_t* gstar,
                                                        int G, int Lp, int radius,
                                                        float inv_norm, float inv_g) {
-  // the block's 256 tokens plus the pooling halo, for every group, in LDS
+  // the block's 256 tokens plus the pooling halo, for up to kAggChunk
+  // subspaces at a time, in LDS (a small tile keeps many blocks per CU when
+  // there is a subspace per head)
   extern __shared__ float tile[];
   const int layer = blockIdx.y;
   const int t0 = blockIdx.x * 256;
   const int span = 256 + 2 * radius;
-  for (int i = threadIdx.x; i < G * span; i += 256) {
-    const int g = i / span, u = t0 - radius + i % span;
-    tile[i] = (u >= 0 && u < Lp) ? sraw[(size_t)(layer * G + g) * Lp + u] : 0.f;
-  }
-  __syncthreads();
   const int t = t0 + threadIdx.x;
-  if (t >= Lp) return;
   float best = -INFINITY, total = 0.f;
   int bg = 0;
-  for (int g = 0; g < G; ++g) {
-    const float* row = tile + g * span + threadIdx.x;
-    float acc = 0.f;
-    for (int j = 0; j <= 2 * radius; ++j) acc += row[j];
-    const float sv = acc * inv_norm;
-    S[(size_t)(layer * G + g) * Lp + t] = sv;
-    total += sv;
-    if (sv > best) { best = sv; bg = g; }
+  for (int g0 = 0; g0 < G; g0 += kAggChunk) {
+    const int ng = min(kAggChunk, G - g0);
+    if (g0 > 0) __syncthreads();   // the previous subspaces are read
+    for (int i = threadIdx.x; i < ng * span; i += 256) {
+      const int g = g0 + i / span, u = t0 - radius + i % span;
+      tile[i] = (u >= 0 && u < Lp) ? sraw[(size_t)(layer * G + g) * Lp + u] : 0.f;
+    }
+    __syncthreads();
+    if (t < Lp) {
+      for (int gi = 0; gi < ng; ++gi) {
+        const int g = g0 + gi;
+        const float* row = tile + gi * span + threadIdx.x;
+        float acc = 0.f;
+        for (int j = 0; j <= 2 * radius; ++j) acc += row[j];
+        const float sv = acc * inv_norm;
+        S[(size_t)(layer * G + g) * Lp + t] = sv;
+        total += sv;
+        if (sv > best) { best = sv; bg = g; }
+      }
+    }
   }
+  if (t >= Lp) return;
   sbar[(size_t)layer * Lp + t] = total * inv_g;
   gstar[(size_t)layer * Lp + t] = (uint8_t)bg;
 }
@@ -98,12 +109,7 @@ int launch_score(const Geometry& g, const starkv_params& p, const void* q,
   const int radius = p.pool_kernel / 2;
   const float inv_norm = 1.0f / ((float)p.pool_kernel * (float)g.hps);
   dim3 ag((g.Lp + 255) / 256, g.n_layers);
-  const size_t lds = (size_t)g.Ns * (256 + 2 * radius) * sizeof(float);
-  // once per process; function-local static initialisation is thread-safe
-  static const hipError_t attr = hipFuncSetAttribute(
-      reinterpret_cast<const void*>(&score_aggregate), hipFuncAttributeMaxDynamicSharedMemorySize,
-      160 * 1024);
-  (void)attr;
+  const size_t lds = (size_t)std::min(g.Ns, kAggChunk) * (256 + 2 * radius) * sizeof(float);
   score_aggregate<<<ag, 256, lds, st>>>(a.sraw, S, sbar, gstar, g.Ns, g.Lp, radius,
                                         inv_norm, 1.0f / (float)g.Ns);
   return (int)hipGetLastError();
