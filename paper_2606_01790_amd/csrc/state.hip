@@ -72,20 +72,47 @@ struct StatsArgs {
   FinalArgs fin;          // the layer's finalize, run by its last block
 };
 
-constexpr int kThreads = 1024;
-constexpr int kWaves = kThreads / 64;
 constexpr int kBatch = 8;                 // loads in flight per thread
 constexpr int kKeyBatch = 8;              // keys per thread per rank-binning step
 constexpr int kLoadBatch = 16;            // loads in flight in the first pass over S
-constexpr int kHistInts = 16384;          // 64 KiB: digit or joint histograms
-constexpr int kKeyCache = 20 * 1024;      // visual keys kept in LDS
-constexpr int kCand = 2048;               // keys in the edges' first-digit buckets
 constexpr int kDirect = 256;              // candidates ranked directly, no more digits
-constexpr int kJointOff = 8192;           // joint histogram slot when digits follow
 constexpr int kTieChunks = 256;           // visual-index chunks for locating tie splits
-static_assert(63 * kTieChunks <= kKeyCache, "tie-split counts live in the key cache");
-constexpr size_t kStatsLds =
-    (size_t)kHistInts * 4 + (size_t)kKeyCache * 4 + (size_t)kCand * 4;
+constexpr int kFirstDigitBins = 4096;     // the 12-bit first digit
+
+// Two block shapes.  The wide one (1024 threads, 152 KiB of LDS) fills a CU
+// and serves calls whose blocks fit on the GPU at once; the narrow one (512
+// threads, 61 KiB) runs two blocks per CU for calls with more blocks than
+// CUs (a subspace per head), and needs n_bins <= kNarrowMaxBins.
+//   kHistInts  digit or joint histograms
+//   kKeyCache  visual keys kept in LDS
+//   kCand      keys in the edges' first-digit buckets
+//   kJointOff  joint histogram slot when digits follow
+//   kMaxTies   tied edges whose split counts live in the key cache
+template <int NT>
+struct StatsShape;
+template <>
+struct StatsShape<1024> {
+  static constexpr int kHistInts = 16384, kKeyCache = 20 * 1024, kCand = 2048,
+                       kJointOff = 8192, kMaxTies = 63;
+};
+constexpr int kNarrowMaxBins = 17;
+template <>
+struct StatsShape<512> {
+  static constexpr int kHistInts = 4096 + kNarrowMaxBins * 256, kKeyCache = 6 * 1024,
+                       kCand = 1024, kJointOff = 4096, kMaxTies = kNarrowMaxBins - 1;
+};
+template <int NT>
+constexpr size_t stats_lds() {
+  using C = StatsShape<NT>;
+  return (size_t)C::kHistInts * 4 + (size_t)C::kKeyCache * 4 + (size_t)C::kCand * 4;
+}
+static_assert(StatsShape<1024>::kMaxTies * kTieChunks <= StatsShape<1024>::kKeyCache,
+              "tie-split counts live in the key cache");
+static_assert(StatsShape<512>::kMaxTies * kTieChunks <= StatsShape<512>::kKeyCache,
+              "tie-split counts live in the key cache");
+static_assert(StatsShape<512>::kJointOff >= (kNarrowMaxBins - 1) * 256 &&
+                  StatsShape<512>::kJointOff >= kFirstDigitBins,
+              "later digits and the first digit fit below the joint histogram");
 
 
 // Sum over the wave's lanes (integers: exact in any order).
@@ -95,7 +122,12 @@ __device__ inline int wave_sum_i(int v) {
   return v;
 }
 
+template <int NT>
 __device__ __forceinline__ void stats_body(const StatsArgs& a) {
+  constexpr int kThreads = NT, kWaves = NT / 64;
+  constexpr int kHistInts = StatsShape<NT>::kHistInts, kKeyCache = StatsShape<NT>::kKeyCache,
+                kCand = StatsShape<NT>::kCand, kJointOff = StatsShape<NT>::kJointOff;
+  constexpr int kScanBins = kFirstDigitBins / NT;   // first-digit bins per thread
   extern __shared__ __align__(16) unsigned char smem[];
   int* hist = reinterpret_cast<int*>(smem);
   uint32_t* kc = reinterpret_cast<uint32_t*>(smem + (size_t)kHistInts * 4);
@@ -547,11 +579,12 @@ __device__ __forceinline__ void stats_body(const StatsArgs& a) {
       }
       __syncthreads();
       if (first) {
-        // block-wide scan over the single histogram: thread owns 4 bins
-        int c[4], sum = 0;
+        // block-wide scan over the single histogram: a thread owns
+        // kScanBins bins
+        int c[kScanBins], sum = 0;
 #pragma unroll
-        for (int j = 0; j < 4; ++j) {
-          c[j] = (4 * tid + j < nb) ? hist[4 * tid + j] : 0;
+        for (int j = 0; j < kScanBins; ++j) {
+          c[j] = (kScanBins * tid + j < nb) ? hist[kScanBins * tid + j] : 0;
           sum += c[j];
         }
         int tot;
@@ -562,9 +595,9 @@ __device__ __forceinline__ void stats_body(const StatsArgs& a) {
           const int r = t_rank[b];
           if (exc <= r && r < exc + sum) {
             int run = exc;
-            for (int j = 0; j < 4; ++j) {
+            for (int j = 0; j < kScanBins; ++j) {
               if (r < run + c[j]) {
-                n_key[b] = t_key[b] | ((uint32_t)(4 * tid + j) << shift);
+                n_key[b] = t_key[b] | ((uint32_t)(kScanBins * tid + j) << shift);
                 n_rank[b] = r - run;
                 n_eq[b] = c[j];
                 break;
@@ -956,7 +989,8 @@ __device__ __forceinline__ void finalize_layer(const FinalArgs& a, int layer, in
 // Every block of a layer counts itself in the layer's state header after
 // its results are out; the last one to arrive runs the layer's finalize and
 // clears the count.  No block waits for another.
-__global__ __launch_bounds__(kThreads) void stats_kernel(StatsArgs a) {
+template <int NT>
+__global__ __launch_bounds__(NT) void stats_kernel(StatsArgs a) {
   __shared__ int last_s;
   const int layer = blockIdx.y;
   StateHeader* hdr = reinterpret_cast<StateHeader*>(a.state + (size_t)layer * a.state_stride);
@@ -967,11 +1001,11 @@ __global__ __launch_bounds__(kThreads) void stats_kernel(StatsArgs a) {
   // here races with nothing.
   if (hdr->magic != kStateMagic || hdr->G != a.G || hdr->frame_cap != a.frame_cap) {
     if (blockIdx.x == 0)
-      for (int i = threadIdx.x; i < a.sc; i += kThreads)
+      for (int i = threadIdx.x; i < a.sc; i += NT)
         a.scal[(size_t)layer * a.sc + i] = __builtin_nanf("");
     return;
   }
-  stats_body(a);
+  stats_body<NT>(a);
   // Thread 0 wrote every value the finalize reads (MI_g or H^); its fence
   // publishes them before it counts the block.
   __syncthreads();
@@ -1040,10 +1074,10 @@ int launch_update_state(const Geometry& g, const starkv_params& p,
     a.sp.off[i + 1] = a.sp.off[i] + spans[i].rows * spans[i].cols;
   }
   // once per process; function-local static initialisation is thread-safe
-  static const hipError_t attr = hipFuncSetAttribute(
-      reinterpret_cast<const void*>(&stats_kernel), hipFuncAttributeMaxDynamicSharedMemorySize,
-      (int)kStatsLds);
-  (void)attr;
+  static const hipError_t attr_wide = hipFuncSetAttribute(
+      reinterpret_cast<const void*>(&stats_kernel<1024>),
+      hipFuncAttributeMaxDynamicSharedMemorySize, (int)stats_lds<1024>());
+  (void)attr_wide;
   FinalArgs& f = a.fin;
   f.scal = scalars;
   f.state = a.state;
@@ -1059,7 +1093,18 @@ int launch_update_state(const Geometry& g, const starkv_params& p,
   f.t_max = p.t_max;
   f.n_warmup = p.n_warmup;
   f.n_ramp = p.n_ramp;
-  stats_kernel<<<dim3(g.Ns + 2, g.n_layers), kThreads, kStatsLds, st>>>(a);
+  // the narrow shape when the blocks do not all fit on the GPU at once
+  // (it runs two per CU) and the bins allow it
+  int dev = 0, n_cu = 0;
+  if (hipGetDevice(&dev) != hipSuccess ||
+      hipDeviceGetAttribute(&n_cu, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
+      n_cu <= 0)
+    return (int)hipErrorInvalidDevice;
+  const dim3 grid(g.Ns + 2, g.n_layers);
+  if ((long)grid.x * grid.y > n_cu && p.n_bins <= kNarrowMaxBins)
+    stats_kernel<512><<<grid, 512, stats_lds<512>(), st>>>(a);
+  else
+    stats_kernel<1024><<<grid, 1024, stats_lds<1024>(), st>>>(a);
   return (int)hipGetLastError();
 }
 

@@ -41,13 +41,33 @@ needs_hipcc = pytest.mark.skipif(not (os.path.exists(B.HIPCC) or shutil.which("h
                                  reason="hipcc not available")
 
 
+def _shape(src: str, nt: int) -> int:
+    """Dynamic LDS bytes of the statistics kernel's block shape `nt`, from
+    the StatsShape specialisation in the source."""
+    consts = {m.group(1): int(m.group(2))
+              for m in re.finditer(r"constexpr int (k\w+) = (\d+);", src)}
+    body = src.split("struct StatsShape<%d> {" % nt, 1)[1].split("};", 1)[0]
+
+    def value(name):
+        expr = re.search(name + r" = ([^,;]+)", body).group(1)
+        for k, v in consts.items():
+            expr = re.sub(r"\b%s\b" % k, str(v), expr)
+        assert re.fullmatch(r"[0-9*+ ]+", expr), expr
+        return eval(expr)
+
+    return 4 * (value("kHistInts") + value("kKeyCache") + value("kCand"))
+
+
 @needs_hipcc
 def test_stats_kernel_lds_fits(tmp_path):
+    """The wide shape fits one block per CU; the narrow one, launched when
+    the blocks outnumber the CUs, must fit two."""
     path = os.path.join(B.CSRC, "state.hip")
     src = open(path).read()
-    dynamic = 4 * (_const(src, "kHistInts") + _const(src, "kKeyCache") + _const(src, "kCand"))
-    static = _static_lds(path, "stats_kernel", tmp_path)
-    assert static + dynamic <= LDS_LIMIT, (static, dynamic)
+    wide = _shape(src, 1024) + _static_lds(path, "stats_kernelILi1024", tmp_path)
+    narrow = _shape(src, 512) + _static_lds(path, "stats_kernelILi512", tmp_path)
+    assert wide <= LDS_LIMIT, wide
+    assert 2 * narrow <= LDS_LIMIT, narrow
 
 
 @needs_hipcc

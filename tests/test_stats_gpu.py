@@ -237,3 +237,31 @@ def test_frame_above_the_fused_path_limit():
     sbar = rng.uniform(1e-4, 1e-2, Lp).astype(np.float32)
     say("above 2^24: inputs generated")
     run_stats("N > 2^24", [S, S2], sbar, spans, 1, sk.params_default(), mi_tol=1e-6)
+
+
+@pytest.mark.parametrize("frames,K,M", [(2, 8, 8), (5, 8, 8), (3, 17, 16), (2, 18, 8)])
+def test_more_blocks_than_cus(frames, K, M):
+    """48 layers of 4 subspaces: 288 statistics blocks, more than the GPU's
+    256 CUs, so the kernel takes its narrow block shape (512 threads, two
+    blocks per CU) when K <= 17, and the wide one at K = 18.  Two 39x69
+    frames keep the keys in the narrow shape's LDS cache, five do not; every
+    layer mixes dense key clusters at the edges, two-level ties and plain
+    random scores."""
+    rng = np.random.default_rng(frames * 100 + K)
+    spans, Lp = layout(frames, 39, 69)
+    is_vis = O.visual_metadata(spans, Lp)[0]
+    vis = np.nonzero(is_vis)[0]
+    n_layers, G = 48, 4
+    steps = []
+    for _ in range(2):
+        S = np.empty((n_layers, G, Lp), np.float32)
+        for layer in range(n_layers):
+            S[layer, 0] = cluster_row(rng, Lp, vis, vis.size // 7, vis.size // 5)
+            S[layer, 1] = np.where(rng.random(Lp) < 0.4, 1e-3, 4e-3).astype(np.float32)
+            S[layer, 2] = rng.lognormal(-7, 1.5, Lp).astype(np.float32)
+            S[layer, 3] = cluster_row(rng, Lp, vis, 0, 700)
+        steps.append(S)
+    p = sk.params_default()
+    p.n_bins, p.grid = K, M
+    sbar = rng.uniform(1e-4, 1e-2, Lp).astype(np.float32)
+    run_stats(f"{n_layers} layers K{K} M{M} {frames} frames", steps, sbar, spans, frames, p)
