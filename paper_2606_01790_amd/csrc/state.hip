@@ -1,7 +1,8 @@
 // Online statistics of one step (sec. 3.4-3.6).
 //
-// stats kernel, grid (G + 2, n_layers), 1024 threads, where G is the call's
-// number of scoring subspaces (the KV groups, or the query heads):
+// stats kernel, grid (G + 2, n_layers), 1024 threads (512 when the blocks
+// outnumber the CUs, see StatsShape), where G is the call's number of
+// scoring subspaces (the KV groups, or the query heads):
 //   block g < G   spatial MI of subspace g (sec. 3.4, Eq. MI);
 //   block G       the AEB statistic of sbar: normalised entropy H^ (sec. 3.6),
 //                 or one minus the normalised peak mass in the confidence
@@ -17,10 +18,12 @@
 // ceil(b N / K), found together by one MSB-first radix select over
 // order-preserving 32-bit keys: the bits every key shares are skipped and
 // the first digit is 12 bits wide (one LDS histogram, block-wide scan).
-// The keys are cached in LDS up to 20K of them; beyond that every pass reads
-// S, walking the visual tokens as one index space with a span cursor.
-// Fused path (the edges' first-digit buckets hold at most 1024 keys, or
-// 10240 when the keys are not cached and the key cache holds candidates):
+// The keys are cached in LDS up to the shape's key cache (20K keys, or 6K
+// in the narrow shape); beyond that every pass reads S, walking the visual
+// tokens as one index space with a span cursor.
+// Fused path (the edges' first-digit buckets hold at most half the
+// candidate area, or half the key cache when the keys are not cached and
+// the key cache holds candidates):
 // the joint histogram pass bins every key outside those buckets (its bin is
 // the number of edges in lower buckets) and keeps the others with their cell
 // and token index; up to 256 of them rank themselves directly, more are
