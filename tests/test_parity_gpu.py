@@ -320,6 +320,24 @@ def test_token_tail_sweep(Lp):
              seed=Lp)
 
 
+@pytest.mark.parametrize("nrb,per_head", [(n, False) for n in range(1, 15)]
+                         + [(n, True) for n in range(2, 15)])
+def test_slab_row_block_sweep(nrb, per_head):
+    """Every row-block count of the persistent pass-2 kernel (bf16, d = 128):
+    with a subspace per group, W = 32*nrb - 8 rows of one head (a padded last
+    row block); with a subspace per head, nrb >= 2 heads of W = 32 rows (one
+    row block each, one output per stage; one head per group is the
+    per-group case).  L_p = 300: four full 64-token slabs
+    and a ragged one."""
+    p = params_for(2, prior_active=True)
+    G = 2
+    H, W = (G * nrb, 32) if per_head else (G, 32 * nrb - 8)
+    Lp = 300
+    spans = [(4, 12, 20, 1)]
+    run_case(f"slab nrb={nrb} per_head={per_head}", H, G, 128, W, Lp + W, spans, 1, 50,
+             "bf16", p, seed=100 + nrb, n_layers=1, per_head=per_head)
+
+
 @pytest.mark.parametrize("k,Lp", [(1, 1), (3, 5), (5, 255), (7, 257), (9, 1025), (63, 700)])
 def test_pool_width_sweep(k, Lp):
     """AvgPool1D widths from 1 to 63 (the widest accepted), with token counts
