@@ -240,6 +240,69 @@ def _decode_unscaled(q, K, V):
     return ORIG["decode_attention"](q * math.sqrt(d), K, V)
 
 
+def _per_head_interleaved(K, H):
+    K = np.asarray(K)
+    return np.tile(K, (H // K.shape[0], 1, 1))     # head h reads group h % G
+
+
+def _discount_variant(linear_unclamped=False, gamma_no_one=False):
+    def f(is_vis, frame, F, phi_of_token, delta, d_min, decay="exp"):
+        if not ((linear_unclamped and decay == "linear") or (gamma_no_one and decay == "gamma")):
+            return ORIG["temporal_discount"](is_vis, frame, F, phi_of_token, delta, d_min, decay)
+        D = np.ones(is_vis.shape[0], dtype=np.float64)
+        dist = (F - frame).astype(np.float64)
+        with np.errstate(divide="ignore"):
+            if decay == "linear":
+                f_ = 1.0 - delta * dist * phi_of_token
+            else:
+                f_ = np.power(dist, -delta * phi_of_token)
+        D_vis = d_min + (1.0 - d_min) * f_
+        D[is_vis] = D_vis[is_vis]
+        return D
+    return f
+
+
+def _confidence_unshifted(sbar, t_min, t_max, eps):
+    p = sbar / (sbar.sum() + eps)
+    c = min(1.0, max(0.0, float(p.max())))
+    return 1.0 - c, t_min + (t_max - t_min) * (1.0 - c)
+
+
+def _confidence_reversed_t(sbar, t_min, t_max, eps):
+    u, _ = ORIG["confidence_temperature"](sbar, t_min, t_max, eps)
+    return u, t_min + (t_max - t_min) * (1.0 - u)
+
+
+def _lambda_ramp_long(n, lam, n_warmup, n_ramp):
+    if n <= n_warmup:
+        return 0.0
+    if n_ramp <= 0:
+        return lam
+    return lam * min(1.0, (n - n_warmup) / (n_ramp + 1))
+
+
+def _gather_window_from_start(K, V, I, L, W):
+    sel = np.concatenate([np.asarray(I, dtype=np.int64), np.arange(W)])
+    return K[:, sel], V[:, sel]
+
+
+def _compress_window_in_softmax(Q, K, V, L, W, spans, F, B, params, state, copy_rows=None):
+    """The softmax runs over all L keys, the window's own included, and the
+    past tokens keep their share."""
+    K_all = np.asarray(K[:, :L], dtype=np.float64)
+    L_p = L - W
+
+    def wam(Q_, K_past):
+        return ORIG["window_attention_mass"](Q_, K_all)[:, :L_p]
+
+    saved = O.window_attention_mass
+    O.window_attention_mass = wam
+    try:
+        return ORIG["compress_layer"](Q, K, V, L, W, spans, F, B, params, state, copy_rows)
+    finally:
+        O.window_attention_mass = saved
+
+
 WAM = ["test_window_rows_sum_to_one", "test_two_key_closed_form_checks_sqrt_d_scaling",
        "test_gqa_head_to_group_map", "test_window_mass_brute_force_tiny",
        "test_zero_queries_give_uniform_mass"]
@@ -298,6 +361,24 @@ MUTANTS = [
     ("topb_select", _topb_high_index, "cut ties keep the higher index", TOPB),
     ("topb_select", _topb_unsorted, "indices not in token order", TOPB),
     ("gather_compact", _gather_no_window, "recent window dropped", ["test_gather_compact_is_row_copy"]),
+    ("per_head_cache", _per_head_interleaved, "per-head cache dealt round-robin",
+     ["test_per_head_cache_gives_each_head_its_own_attention",
+      "test_group_scores_are_means_of_per_head_scores"]),
+    ("temporal_discount", _discount_variant(linear_unclamped=True), "linear decay not floored",
+     [("test_decay_variants_shared_properties", "linear"),
+      "test_decay_variant_closed_forms_and_order"]),
+    ("temporal_discount", _discount_variant(gamma_no_one=True), "gamma decay of the distance, not 1 + distance",
+     [("test_decay_variants_shared_properties", "gamma"),
+      "test_decay_variant_closed_forms_and_order"]),
+    ("confidence_temperature", _confidence_unshifted, "confidence not rescaled from 1/L_p",
+     ["test_confidence_temperature_ends_and_scale_invariance"]),
+    ("confidence_temperature", _confidence_reversed_t, "confidence temperature runs the wrong way",
+     ["test_confidence_temperature_ends_and_scale_invariance"]),
+    ("lambda_schedule", _lambda_ramp_long, "ramp one step too long", ["test_lambda_schedule_values"]),
+    ("gather_compact", _gather_window_from_start, "window rows taken from the cache start",
+     ["test_gather_compact_is_row_copy"]),
+    ("compress_layer", _compress_window_in_softmax, "window keys inside the softmax",
+     ["test_layer_scores_sum_to_the_window_rows"]),
     ("decode_attention", _decode_unscaled, "decode logits not scaled by 1/sqrt(d)",
      ["test_decode_two_tokens_closed_form", "test_decode_brute_force_and_token_permutation"]),
 ]

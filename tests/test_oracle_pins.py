@@ -489,6 +489,17 @@ def test_base_reduction():
     assert list(out["I"]) == sorted(np.argsort(-out["sbar"], kind="stable")[:7])
 
 
+def test_layer_scores_sum_to_the_window_rows():
+    """Sec. 3.3 with the softmax over the L_p past keys: every window row's
+    mass sums to 1 over the past tokens, so with one head per group and a
+    pool of width 1, each group's score row S sums to W exactly (the window's
+    own keys take no share of it)."""
+    Q, K, V, L, W, spans = _tiny_layer(26, H=2, G=2)
+    p = O.Params(pool_kernel=1)
+    out, _ = O.compress_layer(Q, K, V, L, W, spans, 1, 5, p, O.LayerState(2))
+    np.testing.assert_allclose(out["S"].sum(axis=1), [W, W], rtol=1e-12)
+
+
 def test_layer_state_across_steps():
     """Two steps: the counter advances, MI_bar follows the EMA recursion from
     zero, phi is 0 on the first step, and frame-1 tokens get discounted."""
