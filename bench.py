@@ -3,8 +3,9 @@
 
 One bench step is one whole pass of the hot path over the workload: every
 trajectory step of the 28-layer, 5-screenshot trajectory (Qwen2.5-VL-7B
-GQA shape, bf16), each running starkv_score, starkv_update_state,
-starkv_select and starkv_compact for all layers.  The caches of every
+GQA shape, bf16), each running starkv_score, starkv_update_state_select
+(the statistics and the selection in one call) and starkv_compact for all
+layers.  The caches of every
 trajectory step, the window queries and a fresh per-trajectory state are
 resident in HBM before the timed region starts.
 
@@ -168,10 +169,8 @@ class Workload:
             B = sp.budgets(s)[0]
             sk.score(dims, p, self.Q[i], self.K[i], self.layout[i], self.S, self.sbar,
                      self.gstar, self.ws)
-            sk.update_state(dims, p, self.S, self.sbar, spans, s, state, self.frame_cap,
-                            self.scal, self.ws)
-            sk.select(dims, p, self.sbar, self.gstar, self.scal, spans, s, B, self.s,
-                      self.idx, self.ws)
+            sk.update_state_select(dims, p, self.S, self.sbar, self.gstar, spans, s, state,
+                                   self.frame_cap, self.scal, B, self.s, self.idx, self.ws)
             sk.compact(dims, self.K[i], self.V[i], self.layout[i], self.idx, B, self.k_out,
                        self.v_out)
 
@@ -189,6 +188,9 @@ def call_bytes(spec, s, name, per_head=False):
         per = 4 * Ns * nv + 4 * Lp + 4 * Ns * nf * 3
     elif name == "select":     # sbar, g* in; s, idx out
         per = 5 * Lp + 4 * Lp + 4 * B
+    elif name == "update_state_select":
+        return call_bytes(spec, s, "update_state", per_head) + call_bytes(spec, s, "select",
+                                                                          per_head)
     else:                      # idx in; B+W rows of K and V in and out
         per = 4 * B + 4 * G * (B + W) * d * e
     return nl * per
@@ -227,6 +229,9 @@ def per_call_timing(wl, spec, sk, torch, reps):
                                                     scratch, wl.frame_cap, wl.scal, wl.ws),
             "select": lambda: sk.select(dims, p, wl.sbar, wl.gstar, wl.scal, spans, s, B,
                                         wl.s, wl.idx, wl.ws),
+            "update_state_select": lambda: sk.update_state_select(
+                dims, p, wl.S, wl.sbar, wl.gstar, spans, s, scratch, wl.frame_cap, wl.scal, B,
+                wl.s, wl.idx, wl.ws),
             "compact": lambda: sk.compact(dims, wl.K[i], wl.V[i], wl.layout[i], wl.idx, B,
                                           wl.k_out, wl.v_out),
         }

@@ -315,6 +315,25 @@ starkv_status starkv_select(const starkv_dims* dims, const starkv_params* params
                             int32_t frame, int32_t B, float* s, int32_t* idx,
                             void* ws, size_t ws_bytes, void* stream);
 
+/* starkv_update_state followed by starkv_select, in one call (sec. 3.4-3.6,
+ * then sec. 3.2 and 3.7; Algorithm 1, from the statistics through the
+ * selection line): the arguments of both, with the same meaning, layout,
+ * ownership and errors; the outputs (scalars, state, s, idx) are bit for bit
+ * those of the two calls in a row.  Where the statistics run one block per
+ * CU, the block that finishes a layer's statistics runs that layer's
+ * selection next, so the selection needs no launch of its own; otherwise
+ * the two launches are queued.
+ * ws, ws_bytes: unused (reserved); may be NULL and 0.
+ * Errors: E_NULL, E_SHAPE, E_BUDGET, E_SPANS, E_PARAM, E_STATE, E_ALIGN,
+ * E_HIP. */
+starkv_status starkv_update_state_select(const starkv_dims* dims,
+                                         const starkv_params* params, const float* S,
+                                         const float* sbar, const uint8_t* gstar,
+                                         const starkv_span* spans, int32_t n_spans,
+                                         int32_t frame, void* state, int32_t frame_cap,
+                                         float* scalars, int32_t B, float* s, int32_t* idx,
+                                         void* ws, size_t ws_bytes, void* stream);
+
 /* Gather-compaction (sec. 3.7; Algorithm 1, return line), over the G KV
  * groups whatever the subspaces:
  *   K'[g] = [K[g, idx[0..B)]; K[g, L_p..L)],  V' likewise.

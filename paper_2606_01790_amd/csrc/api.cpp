@@ -154,6 +154,33 @@ starkv_status starkv_select(const starkv_dims* dims, const starkv_params* params
                                   frame, B, s, idx, stream));
 }
 
+starkv_status starkv_update_state_select(const starkv_dims* dims,
+                                         const starkv_params* params, const float* S,
+                                         const float* sbar, const uint8_t* gstar,
+                                         const starkv_span* spans, int32_t n_spans,
+                                         int32_t frame, void* state, int32_t frame_cap,
+                                         float* scalars, int32_t B, float* s, int32_t* idx,
+                                         void* ws, size_t ws_bytes, void* stream) {
+  (void)ws;
+  (void)ws_bytes;
+  Geometry g;
+  starkv_status st = check_dims(dims, &g);
+  if (st != STARKV_OK) return st;
+  if ((st = check_params(params)) != STARKV_OK) return st;
+  if (!S || !sbar || !gstar || !state || !scalars || !s) return STARKV_E_NULL;
+  if (B < 0 || B > g.Lp) return STARKV_E_BUDGET;
+  if (B > 0 && !idx) return STARKV_E_NULL;
+  if ((st = check_spans(spans, n_spans, frame, g.Lp)) != STARKV_OK) return st;
+  if (frame_cap < 0 || frame_tokens(spans, n_spans, frame) > frame_cap)
+    return STARKV_E_STATE;
+  if (!aligned(S, 4) || !aligned(sbar, 4) || !aligned(scalars, 4) || !aligned(state, 16) ||
+      !aligned(s, 4) || (idx && !aligned(idx, 4)))
+    return STARKV_E_ALIGN;
+  return hip_status(launch_update_state_select(g, *params, S, sbar, gstar, spans, n_spans,
+                                               frame, state, frame_cap, scalars, B, s, idx,
+                                               stream));
+}
+
 starkv_status starkv_compact(const starkv_dims* dims, const void* k,
                              const void* v, const starkv_kv_layout* kv_layout,
                              const int32_t* idx, int32_t B, void* k_out,

@@ -79,6 +79,13 @@ int launch_select(const Geometry& g, const starkv_params& p, const float* sbar,
                   const uint8_t* gstar, const float* scalars,
                   const starkv_span* spans, int32_t n_spans, int32_t frame,
                   int32_t B, float* s, int32_t* idx, void* stream);
+// update_state then select in one launch where the statistics run their
+// 1024-thread shape (else the two launches).
+int launch_update_state_select(const Geometry& g, const starkv_params& p, const float* S,
+                               const float* sbar, const uint8_t* gstar,
+                               const starkv_span* spans, int32_t n_spans, int32_t frame,
+                               void* state, int32_t frame_cap, float* scalars, int32_t B,
+                               float* s, int32_t* idx, void* stream);
 int launch_compact(const Geometry& g, const void* k, const void* v,
                    const starkv_kv_layout& lay, const int32_t* idx, int32_t B,
                    void* k_out, void* v_out, void* stream);

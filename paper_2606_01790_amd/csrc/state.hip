@@ -36,9 +36,12 @@
 // from per-chunk counts of the equal keys and an ordered scan of one chunk,
 // so that the binning pass itself reads in any order with loads in flight.
 // Either way ties resolve exactly as the ranking defines.
+#include <algorithm>
+
 #include "device_common.h"
 #include "grid_cell.h"
 #include "internal.h"
+#include "select_body.h"
 
 namespace starkv {
 namespace {
@@ -104,6 +107,10 @@ struct StatsShape<512> {
   static constexpr int kHistInts = 4096 + kNarrowMaxBins * 256, kKeyCache = 6 * 1024,
                        kCand = 1024, kJointOff = 4096, kMaxTies = kNarrowMaxBins - 1;
 };
+// The fused selection's key cache follows its fixed LDS in the wide shape's
+// dynamic LDS.
+constexpr size_t kSelKeysOff = (sizeof(SelShared) + 15) / 16 * 16;
+
 template <int NT>
 constexpr size_t stats_lds() {
   using C = StatsShape<NT>;
@@ -113,6 +120,8 @@ static_assert(StatsShape<1024>::kMaxTies * kTieChunks <= StatsShape<1024>::kKeyC
               "tie-split counts live in the key cache");
 static_assert(StatsShape<512>::kMaxTies * kTieChunks <= StatsShape<512>::kKeyCache,
               "tie-split counts live in the key cache");
+static_assert(stats_lds<1024>() >= kSelKeysOff + 4096 * sizeof(uint32_t),
+              "the fused selection's fixed LDS and a key cache fit the wide shape's LDS");
 static_assert(StatsShape<512>::kJointOff >= (kNarrowMaxBins - 1) * 256 &&
                   StatsShape<512>::kJointOff >= kFirstDigitBins,
               "later digits and the first digit fit below the joint histogram");
@@ -992,8 +1001,12 @@ __device__ __forceinline__ void finalize_layer(const FinalArgs& a, int layer, in
 // Every block of a layer counts itself in the layer's state header after
 // its results are out; the last one to arrive runs the layer's finalize and
 // clears the count.  No block waits for another.
-template <int NT>
-__global__ __launch_bounds__(NT) void stats_kernel(StatsArgs a) {
+// With SEL, the block that runs a layer's finalize then runs that layer's
+// selection (select_body) in the same workgroup, its LDS carved from the
+// statistics' dynamic LDS, which no longer holds anything live by then.
+template <int NT, bool SEL>
+__global__ __launch_bounds__(NT) void stats_kernel(StatsArgs a, SelArgs sel) {
+  static_assert(!SEL || NT == kSelThreads, "the selection body needs a 1024-thread block");
   __shared__ int last_s;
   const int layer = blockIdx.y;
   StateHeader* hdr = reinterpret_cast<StateHeader*>(a.state + (size_t)layer * a.state_stride);
@@ -1001,28 +1014,35 @@ __global__ __launch_bounds__(NT) void stats_kernel(StatsArgs a) {
   // frame capacity, or never initialised) is left untouched: the layer's
   // scalars become NaN and no block reads or writes its statistics.  The
   // checked fields are written only by starkv_state_init, so reading them
-  // here races with nothing.
+  // here races with nothing.  With SEL, block 0 then selects on the NaN
+  // scalars, as a separate selection call would.
   if (hdr->magic != kStateMagic || hdr->G != a.G || hdr->frame_cap != a.frame_cap) {
-    if (blockIdx.x == 0)
-      for (int i = threadIdx.x; i < a.sc; i += NT)
-        a.scal[(size_t)layer * a.sc + i] = __builtin_nanf("");
-    return;
+    if (blockIdx.x != 0) return;
+    for (int i = threadIdx.x; i < a.sc; i += NT)
+      a.scal[(size_t)layer * a.sc + i] = __builtin_nanf("");
+  } else {
+    stats_body<NT>(a);
+    // Thread 0 wrote every value the finalize reads (MI_g or H^); its fence
+    // publishes them before it counts the block.
+    __syncthreads();
+    if (threadIdx.x == 0) {
+      __threadfence();
+      last_s = atomicAdd(&hdr->arrive, 1) == a.G + 1;
+    }
+    __syncthreads();
+    if (!last_s) return;
+    if (threadIdx.x < 64) {
+      __threadfence();          // the other blocks' values
+      finalize_layer(a.fin, layer, threadIdx.x);
+    }
+    if (threadIdx.x == 0) hdr->arrive = 0;
   }
-  stats_body<NT>(a);
-  // Thread 0 wrote every value the finalize reads (MI_g or H^); its fence
-  // publishes them before it counts the block.
-  __syncthreads();
-  if (threadIdx.x == 0) {
-    __threadfence();
-    last_s = atomicAdd(&hdr->arrive, 1) == a.G + 1;
+  if constexpr (SEL) {
+    extern __shared__ __align__(16) unsigned char smem_sel[];
+    __syncthreads();   // the layer's scalars are out; the LDS is free
+    select_body(sel, layer, *reinterpret_cast<SelShared*>(smem_sel),
+                reinterpret_cast<uint32_t*>(smem_sel + kSelKeysOff));
   }
-  __syncthreads();
-  if (!last_s) return;
-  if (threadIdx.x < 64) {
-    __threadfence();          // the other blocks' values
-    finalize_layer(a.fin, layer, threadIdx.x);
-  }
-  if (threadIdx.x == 0) hdr->arrive = 0;
 }
 
 __global__ __launch_bounds__(256) void state_init_kernel(char* state, size_t stride,
@@ -1041,14 +1061,9 @@ __global__ __launch_bounds__(256) void state_init_kernel(char* state, size_t str
   }
 }
 
-}  // namespace
-
-int launch_update_state(const Geometry& g, const starkv_params& p,
-                        const float* S, const float* sbar,
-                        const starkv_span* spans, int32_t n_spans,
-                        int32_t frame, void* state, int32_t frame_cap,
-                        float* scalars, void* stream) {
-  hipStream_t st = reinterpret_cast<hipStream_t>(stream);
+StatsArgs make_stats_args(const Geometry& g, const starkv_params& p, const float* S,
+                          const float* sbar, const starkv_span* spans, int32_t n_spans,
+                          int32_t frame, void* state, int32_t frame_cap, float* scalars) {
   StatsArgs a;
   a.S = S;
   a.sbar = sbar;
@@ -1076,11 +1091,6 @@ int launch_update_state(const Geometry& g, const starkv_params& p,
     a.sp.frame[i] = spans[i].frame;
     a.sp.off[i + 1] = a.sp.off[i] + spans[i].rows * spans[i].cols;
   }
-  // once per process; function-local static initialisation is thread-safe
-  static const hipError_t attr_wide = hipFuncSetAttribute(
-      reinterpret_cast<const void*>(&stats_kernel<1024>),
-      hipFuncAttributeMaxDynamicSharedMemorySize, (int)stats_lds<1024>());
-  (void)attr_wide;
   FinalArgs& f = a.fin;
   f.scal = scalars;
   f.state = a.state;
@@ -1096,18 +1106,79 @@ int launch_update_state(const Geometry& g, const starkv_params& p,
   f.t_max = p.t_max;
   f.n_warmup = p.n_warmup;
   f.n_ramp = p.n_ramp;
-  // the narrow shape when the blocks do not all fit on the GPU at once
-  // (it runs two per CU) and the bins allow it
+  return a;
+}
+
+// The wide shape's dynamic LDS is above the default limit; raised once per
+// process (function-local static initialisation is thread-safe).
+void set_wide_lds_attributes() {
+  static const hipError_t attr_plain = hipFuncSetAttribute(
+      reinterpret_cast<const void*>(&stats_kernel<1024, false>),
+      hipFuncAttributeMaxDynamicSharedMemorySize, (int)stats_lds<1024>());
+  static const hipError_t attr_sel = hipFuncSetAttribute(
+      reinterpret_cast<const void*>(&stats_kernel<1024, true>),
+      hipFuncAttributeMaxDynamicSharedMemorySize, (int)stats_lds<1024>());
+  (void)attr_plain;
+  (void)attr_sel;
+}
+
+// 1 for the narrow shape: taken when the blocks do not all fit on the GPU
+// at once (it runs two per CU) and the bins allow it; 0 for the wide one;
+// -1 when the device cannot be queried.
+int use_narrow(const Geometry& g, const starkv_params& p) {
   int dev = 0, n_cu = 0;
   if (hipGetDevice(&dev) != hipSuccess ||
       hipDeviceGetAttribute(&n_cu, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
       n_cu <= 0)
-    return (int)hipErrorInvalidDevice;
+    return -1;
+  return (long)(g.Ns + 2) * g.n_layers > n_cu && p.n_bins <= kNarrowMaxBins ? 1 : 0;
+}
+
+}  // namespace
+
+int launch_update_state(const Geometry& g, const starkv_params& p,
+                        const float* S, const float* sbar,
+                        const starkv_span* spans, int32_t n_spans,
+                        int32_t frame, void* state, int32_t frame_cap,
+                        float* scalars, void* stream) {
+  hipStream_t st = reinterpret_cast<hipStream_t>(stream);
+  const StatsArgs a = make_stats_args(g, p, S, sbar, spans, n_spans, frame, state, frame_cap,
+                                      scalars);
+  set_wide_lds_attributes();
+  const int narrow = use_narrow(g, p);
+  if (narrow < 0) return (int)hipErrorInvalidDevice;
   const dim3 grid(g.Ns + 2, g.n_layers);
-  if ((long)grid.x * grid.y > n_cu && p.n_bins <= kNarrowMaxBins)
-    stats_kernel<512><<<grid, 512, stats_lds<512>(), st>>>(a);
+  SelArgs none{};
+  if (narrow)
+    stats_kernel<512, false><<<grid, 512, stats_lds<512>(), st>>>(a, none);
   else
-    stats_kernel<1024><<<grid, 1024, stats_lds<1024>(), st>>>(a);
+    stats_kernel<1024, false><<<grid, 1024, stats_lds<1024>(), st>>>(a, none);
+  return (int)hipGetLastError();
+}
+
+int launch_update_state_select(const Geometry& g, const starkv_params& p, const float* S,
+                               const float* sbar, const uint8_t* gstar,
+                               const starkv_span* spans, int32_t n_spans, int32_t frame,
+                               void* state, int32_t frame_cap, float* scalars, int32_t B,
+                               float* s, int32_t* idx, void* stream) {
+  hipStream_t st = reinterpret_cast<hipStream_t>(stream);
+  const int narrow = use_narrow(g, p);
+  if (narrow < 0) return (int)hipErrorInvalidDevice;
+  if (narrow) {
+    // the selection needs a 1024-thread block: two launches
+    if (int err = launch_update_state(g, p, S, sbar, spans, n_spans, frame, state, frame_cap,
+                                      scalars, stream))
+      return err;
+    return launch_select(g, p, sbar, gstar, scalars, spans, n_spans, frame, B, s, idx, stream);
+  }
+  const StatsArgs a = make_stats_args(g, p, S, sbar, spans, n_spans, frame, state, frame_cap,
+                                      scalars);
+  SelArgs sel;
+  const long room = (long)((stats_lds<1024>() - kSelKeysOff) / sizeof(uint32_t));
+  fill_sel_args(sel, g, p, sbar, gstar, scalars, spans, n_spans, frame, B, s, idx,
+                (int)std::min<long>({(long)g.Lp, (long)kSelLdsKeys, room}));
+  set_wide_lds_attributes();
+  stats_kernel<1024, true><<<dim3(g.Ns + 2, g.n_layers), 1024, stats_lds<1024>(), st>>>(a, sel);
   return (int)hipGetLastError();
 }
 

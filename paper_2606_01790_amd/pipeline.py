@@ -69,9 +69,9 @@ class LayerGroups:
             if j + 1 < len(self.ranges):
                 prev_scored = torch.cuda.Event()
                 prev_scored.record(st)
-            sk.update_state(dims, params, Sg, sb, spans, step, stg, frame_cap, scg, ws, st)
-            sk.select(dims, params, sb, gs, scg, spans, step, B, s[l0 * Lp:l1 * Lp],
-                      idx[l0 * B:l1 * B] if B else idx, ws, st)
+            sk.update_state_select(dims, params, Sg, sb, gs, spans, step, stg, frame_cap, scg, B,
+                                   s[l0 * Lp:l1 * Lp], idx[l0 * B:l1 * B] if B else idx, ws,
+                                   st)
             sk.compact(dims, kg, vg, lay, idx[l0 * B:l1 * B] if B else idx, B,
                        k_out[l0 * n_out:l1 * n_out], v_out[l0 * n_out:l1 * n_out], st)
         for st in self.streams[1:]:

@@ -95,6 +95,11 @@ SIGNATURES = {
     "starkv_select": (c_int32, [POINTER(Dims), POINTER(Params), c_void_p, c_void_p,
                                 c_void_p, POINTER(Span), c_int32, c_int32, c_int32,
                                 c_void_p, c_void_p, c_void_p, c_size_t, c_void_p]),
+    "starkv_update_state_select": (c_int32, [POINTER(Dims), POINTER(Params), c_void_p,
+                                             c_void_p, c_void_p, POINTER(Span), c_int32,
+                                             c_int32, c_void_p, c_int32, c_void_p, c_int32,
+                                             c_void_p, c_void_p, c_void_p, c_size_t,
+                                             c_void_p]),
     "starkv_compact": (c_int32, [POINTER(Dims), c_void_p, c_void_p,
                                  POINTER(KVLayout), c_void_p, c_int32, c_void_p,
                                  c_void_p, c_void_p]),
@@ -264,6 +269,24 @@ def select(dims: Dims, params: Params, sbar, gstar, scalars, spans, frame: int,
     _check("starkv_select", lib().starkv_select(
         ctypes.byref(dims), ctypes.byref(params), _ptr(sbar), _ptr(gstar),
         _ptr(scalars), arr, n, frame, B, _ptr(s), _ptr(idx), _ptr(ws),
+        0 if ws is None else ws.numel() * ws.element_size(), _stream(stream)))
+
+
+def update_state_select(dims: Dims, params: Params, S, sbar, gstar, spans, frame: int,
+                        state, frame_cap: int, scalars, B: int, s, idx, ws=None,
+                        stream=None):
+    arr, n = spans_array(spans)
+    _need(S, dims.n_layers * dims.Ns * dims.Lp * 4, "S")
+    _need(sbar, dims.n_layers * dims.Lp * 4, "sbar")
+    _need(gstar, dims.n_layers * dims.Lp, "gstar")
+    _need(scalars, dims.n_layers * scalars_count(dims) * 4, "scalars")
+    _need(state, state_bytes(dims, frame_cap), "state")
+    _need(s, dims.n_layers * dims.Lp * 4, "s")
+    if B > 0:
+        _need(idx, dims.n_layers * B * 4, "idx")
+    _check("starkv_update_state_select", lib().starkv_update_state_select(
+        ctypes.byref(dims), ctypes.byref(params), _ptr(S), _ptr(sbar), _ptr(gstar), arr, n,
+        frame, _ptr(state), frame_cap, _ptr(scalars), B, _ptr(s), _ptr(idx), _ptr(ws),
         0 if ws is None else ws.numel() * ws.element_size(), _stream(stream)))
 
 

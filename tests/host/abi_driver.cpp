@@ -23,6 +23,11 @@ int launch_update_state(const Geometry&, const starkv_params&, const float*, con
 int launch_select(const Geometry&, const starkv_params&, const float*, const uint8_t*,
                   const float*, const starkv_span*, int32_t, int32_t, int32_t, float*,
                   int32_t*, void*) { return stub(); }
+int launch_update_state_select(const Geometry&, const starkv_params&, const float*, const float*,
+                               const uint8_t*, const starkv_span*, int32_t, int32_t, void*,
+                               int32_t, float*, int32_t, float*, int32_t*, void*) {
+  return stub();
+}
 int launch_compact(const Geometry&, const void*, const void*, const starkv_kv_layout&,
                    const int32_t*, int32_t, void*, void*, void*) { return stub(); }
 int launch_state_init(const Geometry&, void*, int32_t, void*) { return stub(); }
@@ -69,7 +74,9 @@ int main() {
                                      nullptr), STARKV_OK);
   expect("compact ok", starkv_compact(&d, P, P, &lay, I, 2691, P, P, nullptr), STARKV_OK);
   expect("state init ok", starkv_state_init(&d, P, nf, nullptr), STARKV_OK);
-  expect("launch count", g_launches, 5);
+  expect("update+select ok", starkv_update_state_select(&d, &p, F, F, U, sp.data(), 5, 5, P, nf, F,
+                                                       2691, F, I, nullptr, 0, nullptr), STARKV_OK);
+  expect("launch count", g_launches, 6);
 
   // E_NULL
   expect("score null q", starkv_score(&d, &p, nullptr, P, &lay, F, F, U, P, ws, nullptr), STARKV_E_NULL);
@@ -78,6 +85,15 @@ int main() {
                                           0, nullptr), STARKV_E_NULL);
   expect("update null spans", starkv_update_state(&d, &p, F, F, nullptr, 5, 5, P, nf, F, nullptr, 0,
                                                   nullptr), STARKV_E_NULL);
+  expect("update+select null gstar", starkv_update_state_select(&d, &p, F, F, nullptr, sp.data(), 5, 5,
+                                                              P, nf, F, 10, F, I, nullptr, 0, nullptr),
+         STARKV_E_NULL);
+  expect("update+select null idx", starkv_update_state_select(&d, &p, F, F, U, sp.data(), 5, 5, P, nf,
+                                                             F, 10, F, nullptr, nullptr, 0, nullptr),
+         STARKV_E_NULL);
+  expect("update+select no idx at B = 0", starkv_update_state_select(&d, &p, F, F, U, sp.data(), 5, 5,
+                                                                    P, nf, F, 0, F, nullptr, nullptr,
+                                                                    0, nullptr), STARKV_OK);
   // E_SHAPE
   starkv_dims bad = d;
   bad.H = 30;
@@ -96,6 +112,9 @@ int main() {
   expect("token stride < d", starkv_score(&d, &p, P, P, &short_tok, F, F, U, P, ws, nullptr), STARKV_E_SHAPE);
   // E_BUDGET
   expect("B < 0", starkv_select(&d, &p, F, U, F, sp.data(), 5, 5, -1, F, I, nullptr, 0, nullptr), STARKV_E_BUDGET);
+  expect("update+select B > L_p", starkv_update_state_select(&d, &p, F, F, U, sp.data(), 5, 5, P, nf,
+                                                            F, 13680, F, I, nullptr, 0, nullptr),
+         STARKV_E_BUDGET);
   expect("B > L_p", starkv_compact(&d, P, P, &lay, I, 13680, P, P, nullptr), STARKV_E_BUDGET);
   // E_SPANS
   std::vector<starkv_span> ov = sp;
@@ -110,6 +129,9 @@ int main() {
                                         nullptr), STARKV_E_SPANS);
   expect("too many spans", starkv_update_state(&d, &p, F, F, sp.data(), 65, 5, P, nf, F, nullptr, 0,
                                                nullptr), STARKV_E_SPANS);
+  expect("update+select span past L_p",
+         starkv_update_state_select(&d, &p, F, F, U, past.data(), 5, 5, P, nf, F, 10, F, I, nullptr, 0,
+                                    nullptr), STARKV_E_SPANS);
   // E_PARAM
   starkv_params q = p;
   q.lam = 1.5f;
@@ -142,6 +164,9 @@ int main() {
   // E_STATE
   expect("frame above capacity", starkv_update_state(&d, &p, F, F, sp.data(), 5, 5, P, nf - 1, F,
                                                      nullptr, 0, nullptr), STARKV_E_STATE);
+  expect("update+select frame above capacity",
+         starkv_update_state_select(&d, &p, F, F, U, sp.data(), 5, 5, P, nf - 1, F, 10, F, I, nullptr,
+                                    0, nullptr), STARKV_E_STATE);
   expect("negative capacity", starkv_state_init(&d, P, -1, nullptr), STARKV_E_STATE);
   // E_HIP: a launch that reports an error
   g_fail_launch = 1;

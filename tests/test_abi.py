@@ -32,7 +32,7 @@ def declared_functions():
 def test_header_symbols_are_exported():
     L = sk.lib()
     names = declared_functions()
-    assert len(names) == 14
+    assert len(names) == 15
     for n in names:
         assert hasattr(L, n), n
     assert set(names) == set(sk.SIGNATURES)
@@ -204,6 +204,37 @@ def test_select_and_compact_reject_bad_budget():
     rc = L.starkv_compact(ctypes.byref(d), FAKE, FAKE, ctypes.byref(lay), FAKE, 5,
                           FAKE + 4, FAKE, None)
     assert sk.STATUS[rc] == "E_ALIGN"
+
+
+def _update_select(d, spans, frame, B=5, cap=2691, p=None, S=FAKE, gstar=FAKE, s=FAKE,
+                   idx=FAKE):
+    p = p or sk.params_default()
+    arr, n = sk.spans_array(spans)
+    return sk.STATUS[sk.lib().starkv_update_state_select(
+        ctypes.byref(d), ctypes.byref(p), S, FAKE, gstar, arr, n, frame, FAKE, cap, FAKE, B,
+        s, idx, None, 0, None)]
+
+
+def test_update_state_select_validates_both_argument_lists():
+    """The combined call rejects what either call rejects, before any launch."""
+    d = dims(L=2947)                         # L_p = 2915
+    ok = [(0, 39, 69, 1)]
+    for B in (-1, 2916):
+        assert _update_select(d, ok, 1, B=B) == "E_BUDGET"
+    assert _update_select(d, ok, 1, B=5, idx=None) == "E_NULL"
+    assert _update_select(d, ok, 1, S=None) == "E_NULL"
+    assert _update_select(d, ok, 1, gstar=None) == "E_NULL"
+    assert _update_select(d, ok, 1, s=None) == "E_NULL"
+    assert _update_select(d, [(0, 39, 69, 1)], 2) == "E_SPANS"
+    assert _update_select(d, [(300, 39, 69, 1)], 1) == "E_SPANS"
+    assert _update_select(d, ok, 1, cap=100) == "E_STATE"
+    assert _update_select(d, ok, 1, s=FAKE + 2) == "E_ALIGN"
+    p = sk.params_default()
+    p.tau = 0.0
+    assert _update_select(d, ok, 1, p=p) == "E_PARAM"
+    bad = dims(L=2947)
+    bad.G = 3                                # H % G != 0
+    assert _update_select(bad, ok, 1) == "E_SHAPE"
 
 
 def test_state_init_rejects():

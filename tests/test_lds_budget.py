@@ -64,16 +64,18 @@ def test_stats_kernel_lds_fits(tmp_path):
     the blocks outnumber the CUs, must fit two."""
     path = os.path.join(B.CSRC, "state.hip")
     src = open(path).read()
-    wide = _shape(src, 1024) + _static_lds(path, "stats_kernelILi1024", tmp_path)
+    for fused in ("0", "1"):
+        wide = _shape(src, 1024) + _static_lds(path, "stats_kernelILi1024ELb%sE" % fused,
+                                               tmp_path)
+        assert wide <= LDS_LIMIT, (fused, wide)
     narrow = _shape(src, 512) + _static_lds(path, "stats_kernelILi512", tmp_path)
-    assert wide <= LDS_LIMIT, wide
     assert 2 * narrow <= LDS_LIMIT, narrow
 
 
 @needs_hipcc
 def test_select_kernel_lds_fits(tmp_path):
     path = os.path.join(B.CSRC, "select.hip")
-    src = open(path).read()
-    dynamic = 4 * _const(src, "kLdsKeys")
+    src = open(os.path.join(B.CSRC, "select_body.h")).read()
+    dynamic = 4 * _const(src, "kSelLdsKeys")
     static = _static_lds(path, "select_kernel", tmp_path)
     assert static + dynamic <= LDS_LIMIT, (static, dynamic)
