@@ -172,10 +172,23 @@ class TrajectoryRunner:
         sk.compact(dims, self.K, self.V, self.layout, self.idx, B, self.k_out,
                    self.v_out, stream)
 
-    def run_step(self, step: int, B: int, stream=None, groups: int = 1):
-        """The compression stage of one step for all layers: the four calls,
+    def run_step(self, step: int, B: int, stream=None, groups: int = 1, fused: bool = False):
+        """The compression stage of one step for all layers: the four calls
+        (three with `fused`: the statistics and the selection in one call),
         on the current stream, or as `groups` layer groups on as many streams
         (see LayerGroups)."""
+        if groups <= 1 and fused:
+            sp = self.spec
+            dims = self.dims(step)
+            spans = sp.spans(step)
+            sk.score(dims, self.params, self.Q, self.K, self.layout, self.S, self.sbar,
+                     self.gstar, self.ws, stream)
+            sk.update_state_select(dims, self.params, self.S, self.sbar, self.gstar, spans, step,
+                                   self.state, self.frame_cap, self.scal, B, self.s, self.idx,
+                                   self.ws, stream)
+            sk.compact(dims, self.K, self.V, self.layout, self.idx, B, self.k_out, self.v_out,
+                       stream)
+            return
         if groups <= 1:
             self.score_and_update(step, stream)
             self.select_and_compact(step, B, stream)

@@ -231,27 +231,29 @@ def test_determinism_bitwise():
         assert np.array_equal(outs[0][k], outs[1][k]), k
 
 
-def test_graph_replay_matches_eager():
-    """A two-step trajectory (fresh state, four calls per step) captured into a
-    HIP graph: every replay, with eager work between replays, reproduces the
-    eager run bit for bit."""
+@pytest.mark.parametrize("fused", [False, True])
+def test_graph_replay_matches_eager(fused):
+    """A trajectory step (fresh state, four calls, or three with the
+    statistics and the selection in one call) captured into a HIP graph:
+    every replay, with eager work between replays, reproduces the eager run
+    of the four separate calls bit for bit."""
     spec = WL.SPECS[3]
     p = params_for(3, prior_active=True)
     r = TrajectoryRunner(spec, p)
     for s in (1, 2):
         r.load_step(s)     # caches hold step 2's text; step 1 only reads frame 1 + text
-    # eager reference: steps 1 and 2 on the same buffers as the graph
-    def traj():
+    # eager reference: the separate calls on the same buffers as the graph
+    def traj(fused_calls):
         sk.state_init(r.dims(spec.peak_step), r.state, r.frame_cap)
-        r.run_step(2, spec.budgets(2)[0])
-    say("graph: eager reference")
-    traj()
+        r.run_step(2, spec.budgets(2)[0], fused=fused_calls)
+    say(f"graph (fused {fused}): eager reference")
+    traj(False)
     torch.cuda.synchronize()
     ref = r.outputs(2, spec.budgets(2)[0])
     g = torch.cuda.CUDAGraph()
     say("graph: capture")
     with torch.cuda.graph(g):
-        traj()
+        traj(fused)
     for rep in range(3):
         r.S.zero_()
         r.s.zero_()
@@ -264,7 +266,7 @@ def test_graph_replay_matches_eager():
         out = r.outputs(2, spec.budgets(2)[0])
         for k in ref:
             assert np.array_equal(ref[k], out[k]), (rep, k)
-        traj()                       # eager work between replays
+        traj(fused)                  # eager work between replays
         torch.cuda.synchronize()
 
 
