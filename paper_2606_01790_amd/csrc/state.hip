@@ -1,7 +1,7 @@
 // Online statistics of one step (sec. 3.4-3.6).
 //
-// stats kernel, grid (G + 2, n_layers), 1024 threads (512 when the blocks
-// outnumber the CUs, see StatsShape), where G is the call's number of
+// stats kernel, grid (G + 2, n_layers), 1024 threads (512 or 256 when the
+// blocks outnumber the CUs, see StatsShape), where G is the call's number of
 // scoring subspaces (the KV groups, or the query heads):
 //   block g < G   spatial MI of subspace g (sec. 3.4, Eq. MI);
 //   block G       the AEB statistic of sbar: normalised entropy H^ (sec. 3.6),
@@ -18,9 +18,9 @@
 // ceil(b N / K), found together by one MSB-first radix select over
 // order-preserving 32-bit keys: the bits every key shares are skipped and
 // the first digit is 12 bits wide (one LDS histogram, block-wide scan).
-// The keys are cached in LDS up to the shape's key cache (20K keys, or 6K
-// in the narrow shape); beyond that every pass reads S, walking the visual
-// tokens as one index space with a span cursor.
+// The keys are cached in LDS up to the shape's key cache (20K keys, 6K in
+// the narrow shape, 2K in the small one); beyond that every pass reads S,
+// walking the visual tokens as one index space with a span cursor.
 // Fused path (the edges' first-digit buckets hold at most half the
 // candidate area, or half the key cache when the keys are not cached and
 // the key cache holds candidates):
@@ -85,10 +85,13 @@ constexpr int kDirect = 256;              // candidates ranked directly, no more
 constexpr int kTieChunks = 256;           // visual-index chunks for locating tie splits
 constexpr int kFirstDigitBins = 4096;     // the 12-bit first digit
 
-// Two block shapes.  The wide one (1024 threads, 152 KiB of LDS) fills a CU
-// and serves calls whose blocks fit on the GPU at once; the narrow one (512
-// threads, 61 KiB) runs two blocks per CU for calls with more blocks than
-// CUs (a subspace per head), and needs n_bins <= kNarrowMaxBins.
+// Three block shapes.  The wide one (1024 threads, 152 KiB of LDS) fills a
+// CU and serves calls whose blocks fit on the GPU at once; the narrow one
+// (512 threads, 61 KiB) runs two blocks per CU for calls with more blocks
+// than CUs (a subspace per head), and needs n_bins <= kNarrowMaxBins; the
+// small one (256 threads, 29 KiB, at most 128 VGPRs) runs four per CU for
+// calls with more blocks than two per CU, and needs n_bins <= kSmallMaxBins
+// and grid^2 <= kSmallMaxCells.
 //   kHistInts  digit or joint histograms
 //   kKeyCache  visual keys kept in LDS
 //   kCand      keys in the edges' first-digit buckets
@@ -107,6 +110,13 @@ struct StatsShape<512> {
   static constexpr int kHistInts = 4096 + kNarrowMaxBins * 256, kKeyCache = 6 * 1024,
                        kCand = 1024, kJointOff = 4096, kMaxTies = kNarrowMaxBins - 1;
 };
+constexpr int kSmallMaxBins = 9;
+constexpr int kSmallMaxCells = 64;
+template <>
+struct StatsShape<256> {
+  static constexpr int kHistInts = 4096 + kSmallMaxBins * kSmallMaxCells, kKeyCache = 2048,
+                       kCand = 512, kJointOff = 4096, kMaxTies = kSmallMaxBins - 1;
+};
 // The fused selection's key cache follows its fixed LDS in the wide shape's
 // dynamic LDS.
 constexpr size_t kSelKeysOff = (sizeof(SelShared) + 15) / 16 * 16;
@@ -120,6 +130,12 @@ static_assert(StatsShape<1024>::kMaxTies * kTieChunks <= StatsShape<1024>::kKeyC
               "tie-split counts live in the key cache");
 static_assert(StatsShape<512>::kMaxTies * kTieChunks <= StatsShape<512>::kKeyCache,
               "tie-split counts live in the key cache");
+static_assert(StatsShape<256>::kMaxTies * kTieChunks <= StatsShape<256>::kKeyCache,
+              "tie-split counts live in the key cache");
+static_assert(kDirect <= 256 && StatsShape<256>::kJointOff >= (kSmallMaxBins - 1) * 256 &&
+                  StatsShape<256>::kJointOff >= kFirstDigitBins,
+              "direct ranking has a thread per candidate; the digits fit below the joint "
+              "histogram");
 static_assert(stats_lds<1024>() >= kSelKeysOff + 4096 * sizeof(uint32_t),
               "the fused selection's fixed LDS and a key cache fit the wide shape's LDS");
 static_assert(StatsShape<512>::kJointOff >= (kNarrowMaxBins - 1) * 256 &&
@@ -1005,7 +1021,7 @@ __device__ __forceinline__ void finalize_layer(const FinalArgs& a, int layer, in
 // selection (select_body) in the same workgroup, its LDS carved from the
 // statistics' dynamic LDS, which no longer holds anything live by then.
 template <int NT, bool SEL>
-__global__ __launch_bounds__(NT) void stats_kernel(StatsArgs a, SelArgs sel) {
+__global__ __launch_bounds__(NT, 1024 / NT) void stats_kernel(StatsArgs a, SelArgs sel) {
   static_assert(!SEL || NT == kSelThreads, "the selection body needs a 1024-thread block");
   __shared__ int last_s;
   const int layer = blockIdx.y;
@@ -1122,16 +1138,22 @@ void set_wide_lds_attributes() {
   (void)attr_sel;
 }
 
-// 1 for the narrow shape: taken when the blocks do not all fit on the GPU
-// at once (it runs two per CU) and the bins allow it; 0 for the wide one;
-// -1 when the device cannot be queried.
-int use_narrow(const Geometry& g, const starkv_params& p) {
+// The statistics block shape (threads per block) for this call: the wide
+// one when the blocks all fit on the GPU at once (one per CU) or the bins
+// need it, else the narrow one (two per CU), or the small one (four per CU)
+// when even two per CU leave blocks for a second round and the bins and
+// cells allow it; -1 when the device cannot be queried.
+int stats_shape(const Geometry& g, const starkv_params& p) {
   int dev = 0, n_cu = 0;
   if (hipGetDevice(&dev) != hipSuccess ||
       hipDeviceGetAttribute(&n_cu, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
       n_cu <= 0)
     return -1;
-  return (long)(g.Ns + 2) * g.n_layers > n_cu && p.n_bins <= kNarrowMaxBins ? 1 : 0;
+  const long blocks = (long)(g.Ns + 2) * g.n_layers;
+  if (blocks <= n_cu || p.n_bins > kNarrowMaxBins) return 1024;
+  if (blocks > 2L * n_cu && p.n_bins <= kSmallMaxBins && p.grid * p.grid <= kSmallMaxCells)
+    return 256;
+  return 512;
 }
 
 }  // namespace
@@ -1145,11 +1167,13 @@ int launch_update_state(const Geometry& g, const starkv_params& p,
   const StatsArgs a = make_stats_args(g, p, S, sbar, spans, n_spans, frame, state, frame_cap,
                                       scalars);
   set_wide_lds_attributes();
-  const int narrow = use_narrow(g, p);
-  if (narrow < 0) return (int)hipErrorInvalidDevice;
+  const int nt = stats_shape(g, p);
+  if (nt < 0) return (int)hipErrorInvalidDevice;
   const dim3 grid(g.Ns + 2, g.n_layers);
   SelArgs none{};
-  if (narrow)
+  if (nt == 256)
+    stats_kernel<256, false><<<grid, 256, stats_lds<256>(), st>>>(a, none);
+  else if (nt == 512)
     stats_kernel<512, false><<<grid, 512, stats_lds<512>(), st>>>(a, none);
   else
     stats_kernel<1024, false><<<grid, 1024, stats_lds<1024>(), st>>>(a, none);
@@ -1162,9 +1186,9 @@ int launch_update_state_select(const Geometry& g, const starkv_params& p, const 
                                void* state, int32_t frame_cap, float* scalars, int32_t B,
                                float* s, int32_t* idx, void* stream) {
   hipStream_t st = reinterpret_cast<hipStream_t>(stream);
-  const int narrow = use_narrow(g, p);
-  if (narrow < 0) return (int)hipErrorInvalidDevice;
-  if (narrow) {
+  const int nt = stats_shape(g, p);
+  if (nt < 0) return (int)hipErrorInvalidDevice;
+  if (nt != 1024) {
     // the selection needs a 1024-thread block: two launches
     if (int err = launch_update_state(g, p, S, sbar, spans, n_spans, frame, state, frame_cap,
                                       scalars, stream))

@@ -61,7 +61,7 @@ def _shape(src: str, nt: int) -> int:
 @needs_hipcc
 def test_stats_kernel_lds_fits(tmp_path):
     """The wide shape fits one block per CU; the narrow one, launched when
-    the blocks outnumber the CUs, must fit two."""
+    the blocks outnumber the CUs, must fit two, and the small one four."""
     path = os.path.join(B.CSRC, "state.hip")
     src = open(path).read()
     for fused in ("0", "1"):
@@ -70,6 +70,8 @@ def test_stats_kernel_lds_fits(tmp_path):
         assert wide <= LDS_LIMIT, (fused, wide)
     narrow = _shape(src, 512) + _static_lds(path, "stats_kernelILi512", tmp_path)
     assert 2 * narrow <= LDS_LIMIT, narrow
+    small = _shape(src, 256) + _static_lds(path, "stats_kernelILi256", tmp_path)
+    assert 4 * small <= LDS_LIMIT, small
 
 
 @needs_hipcc

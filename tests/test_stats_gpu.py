@@ -239,19 +239,24 @@ def test_frame_above_the_fused_path_limit():
     run_stats("N > 2^24", [S, S2], sbar, spans, 1, sk.params_default(), mi_tol=1e-6)
 
 
-@pytest.mark.parametrize("frames,K,M", [(2, 8, 8), (5, 8, 8), (3, 17, 16), (2, 18, 8)])
-def test_more_blocks_than_cus(frames, K, M):
+@pytest.mark.parametrize("frames,K,M,n_layers", [
+    (2, 8, 8, 48), (5, 8, 8, 48), (3, 17, 16, 48), (2, 18, 8, 48),
+    (2, 8, 8, 96), (5, 9, 8, 96), (1, 2, 2, 96), (3, 10, 8, 96), (2, 8, 16, 96)])
+def test_more_blocks_than_cus(frames, K, M, n_layers):
     """48 layers of 4 subspaces: 288 statistics blocks, more than the GPU's
     256 CUs, so the kernel takes its narrow block shape (512 threads, two
-    blocks per CU) when K <= 17, and the wide one at K = 18.  Two 39x69
-    frames keep the keys in the narrow shape's LDS cache, five do not; every
+    blocks per CU) when K <= 17, and the wide one at K = 18.  96 layers: 576
+    blocks, more than two per CU, so the small shape (256 threads, four per
+    CU) when K <= 9 and M*M <= 64, else the narrow one (K = 10, or M = 16).
+    One or two 39x69 frames keep the keys in the narrow shape's LDS cache
+    (the small shape's 2K-key cache holds none of them), five do not; every
     layer mixes dense key clusters at the edges, two-level ties and plain
     random scores."""
-    rng = np.random.default_rng(frames * 100 + K)
+    rng = np.random.default_rng(frames * 100 + K + n_layers)
     spans, Lp = layout(frames, 39, 69)
     is_vis = O.visual_metadata(spans, Lp)[0]
     vis = np.nonzero(is_vis)[0]
-    n_layers, G = 48, 4
+    G = 4
     steps = []
     for _ in range(2):
         S = np.empty((n_layers, G, Lp), np.float32)
