@@ -14,6 +14,10 @@ namespace {
 // subspaces, g* = first argmax.  The pooled sum adds the k window values in
 // token order; the mean and the argmax take the subspaces in order.
 constexpr int kAggChunk = 8;   // subspaces per LDS tile
+constexpr int kAggMaxRadius = 31;   // pool widths up to 63
+// loads per thread that fill one tile: every one is issued before the first
+// LDS store, so a tile costs one round trip
+constexpr int kAggLoads = (kAggChunk * (256 + 2 * kAggMaxRadius) + 255) / 256;
 
 __global__ __launch_bounds__(256) void score_aggregate(const float* sraw, float* S,
                                                        float* sbar, uint8_t* gstar,
@@ -31,10 +35,18 @@ __global__ __launch_bounds__(256) void score_aggregate(const float* sraw, float*
   int bg = 0;
   for (int g0 = 0; g0 < G; g0 += kAggChunk) {
     const int ng = min(kAggChunk, G - g0);
-    if (g0 > 0) __syncthreads();   // the previous subspaces are read
-    for (int i = threadIdx.x; i < ng * span; i += 256) {
+    float v[kAggLoads];
+#pragma unroll
+    for (int j = 0; j < kAggLoads; ++j) {
+      const int i = threadIdx.x + j * 256;
       const int g = g0 + i / span, u = t0 - radius + i % span;
-      tile[i] = (u >= 0 && u < Lp) ? sraw[(size_t)(layer * G + g) * Lp + u] : 0.f;
+      v[j] = (i < ng * span && u >= 0 && u < Lp) ? sraw[(size_t)(layer * G + g) * Lp + u] : 0.f;
+    }
+    if (g0 > 0) __syncthreads();   // the previous subspaces are read
+#pragma unroll
+    for (int j = 0; j < kAggLoads; ++j) {
+      const int i = threadIdx.x + j * 256;
+      if (i < ng * span) tile[i] = v[j];
     }
     __syncthreads();
     if (t < Lp) {
@@ -107,6 +119,7 @@ int launch_score(const Geometry& g, const starkv_params& p, const void* q,
                                          : run_score_f32(a, g.d, g.n_layers, st);
   if (err) return err;
   const int radius = p.pool_kernel / 2;
+  if (radius > kAggMaxRadius) return (int)hipErrorInvalidValue;   // validated before
   const float inv_norm = 1.0f / ((float)p.pool_kernel * (float)g.hps);
   dim3 ag((g.Lp + 255) / 256, g.n_layers);
   const size_t lds = (size_t)std::min(g.Ns, kAggChunk) * (256 + 2 * radius) * sizeof(float);
