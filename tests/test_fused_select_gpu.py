@@ -8,7 +8,8 @@ cover the fused shape (one block per CU, the selection in the finalizing
 block), its LDS key cache (a prefix of L_p that is smaller than the
 selection kernel's own), budgets 0 and L_p, the narrow-shape and per-head
 fallbacks (two launches), frames of changing size (the stability means
-restart), and a layer whose state block does not match (NaN scalars).  The
+restart), a layer whose state block does not match (NaN scalars), and the
+temporal-decay and AEB variants.  The
 oracle parity of each half is covered by the statistics and selection
 tests; this one pins the fusion.
 """
@@ -151,3 +152,18 @@ def test_fused_mismatched_state_layer():
     spans, Lp = layout(2, 23, 31)
     run_pair("spoiled layer", 8, 8, 2, [(spans, 2, Lp)] * 2, B=Lp // 4, spoil_layer=3,
              seed=17)
+
+
+@pytest.mark.parametrize("tem,aeb", [("linear", "entropy"), ("gamma", "confidence"),
+                                     ("exp", "confidence")])
+def test_fused_ablation_variants(tem, aeb):
+    """The temporal-decay and AEB variants (the discount table and the
+    temperature of the fused selection), with the prior active from the
+    first step."""
+    spans, Lp = layout(4, 39, 69)
+    p = sk.params_default()
+    p.tem_decay = sk.TEM_DECAY[tem]
+    p.aeb_mode = sk.AEB_MODE[aeb]
+    p.n_warmup, p.n_ramp = 0, 0
+    steps = [(spans[:f], f, Lp) for f in (2, 3, 4)]
+    run_pair(f"{tem}/{aeb}", 28, 28, 4, steps, B=Lp // 4, p=p, seed=19)
