@@ -672,3 +672,52 @@ def test_no_visual_spans():
     _, states = run_case("no spans", 8, 2, 64, 8, 500, [], 0, 80, "bf16", p, seed=63)
     for st in states:
         assert np.all(st.mi_bar == 0.0)
+
+
+def _random_configuration(seed):
+    """A seeded draw over the ABI's shapes and parameters: dtype, head size,
+    groups and heads per group, window, subspace granularity, frames with
+    text between them, budget, bins, grid, pooling width, the decay and AEB
+    variants and whether the prior is active.  Shapes the ABI rejects are
+    redrawn."""
+    rng = np.random.default_rng(7000 + seed)
+    while True:
+        dtype = "f32" if rng.random() < 0.25 else "bf16"
+        d = int(rng.choice([64, 128]))
+        G = int(rng.choice([1, 2, 4, 8]))
+        hpg = int(rng.choice([1, 2, 4, 7]))
+        W = int(rng.choice([8, 16, 24, 32, 40]))
+        per_head = bool(rng.random() < 0.3)
+        H = G * hpg
+        Rpad = (W * hpg + 31) // 32 * 32
+        esz = 4 if dtype == "f32" else 2
+        if Rpad > (128 if dtype == "f32" else 512) or Rpad * (d * esz + 16) > 128 * 1024:
+            continue
+        break
+    spans, t = [], int(rng.integers(0, 40))
+    for f in range(1, int(rng.integers(1, 5)) + 1):
+        rows, cols = int(rng.integers(2, 30)), int(rng.integers(2, 40))
+        spans.append((t, rows, cols, f))
+        t += rows * cols + int(rng.integers(0, 60))
+    Lp = t + int(rng.integers(1, 50))
+    p = sk.params_default()
+    p.n_bins = int(rng.integers(1, 21))
+    p.grid = int(rng.integers(1, 13))
+    p.pool_kernel = int(rng.choice([1, 3, 5, 7, 9, 15]))
+    p.tem_decay = sk.TEM_DECAY[str(rng.choice(list(sk.TEM_DECAY)))]
+    p.aeb_mode = sk.AEB_MODE[str(rng.choice(list(sk.AEB_MODE)))]
+    if rng.random() < 0.5:
+        p.n_warmup, p.n_ramp = 0, 0
+    B = int(rng.integers(0, Lp + 1))
+    return dict(H=H, G=G, d=d, W=W, L=Lp + W, spans=spans, F=len(spans), B=B,
+                dtype=dtype, p=p, per_head=per_head)
+
+
+@pytest.mark.parametrize("seed", range(48))
+def test_random_configurations(seed):
+    """Forty-eight seeded configurations drawn over shapes and parameters, each
+    compared with the oracle on two layers at the same bar as the targeted
+    cases."""
+    c = _random_configuration(seed)
+    run_case(f"random {seed}", c["H"], c["G"], c["d"], c["W"], c["L"], c["spans"], c["F"],
+             c["B"], c["dtype"], c["p"], seed=seed, per_head=c["per_head"])
