@@ -721,3 +721,30 @@ def test_random_configurations(seed):
     c = _random_configuration(seed)
     run_case(f"random {seed}", c["H"], c["G"], c["d"], c["W"], c["L"], c["spans"], c["F"],
              c["B"], c["dtype"], c["p"], seed=seed, per_head=c["per_head"])
+
+
+@pytest.mark.parametrize("seed", range(12))
+def test_random_trajectories(seed):
+    """Twelve seeded three-step trajectories: a random configuration whose
+    frames arrive one per step (sizes may differ from frame to frame), the
+    layer state carried on the GPU and in the oracle, every step compared."""
+    c = _random_configuration(100 + seed)
+    rng = np.random.default_rng(9000 + seed)
+    spans, t = [], int(rng.integers(0, 40))
+    for f in range(1, 4):
+        rows, cols = int(rng.integers(2, 30)), int(rng.integers(2, 40))
+        spans.append((t, rows, cols, f))
+        t += rows * cols + int(rng.integers(0, 60))
+    L_cap = t + int(rng.integers(1, 50)) + c["W"]
+    frame_cap = max(r * cc for (_, r, cc, _) in spans)
+    case = ArrayCase(c["H"], c["G"], c["d"], c["W"], 2, L_cap, c["dtype"], c["p"], frame_cap,
+                     per_head=c["per_head"])
+    states = None
+    for step in range(1, 4):
+        cur = spans[:step]
+        L = cur[-1][0] + cur[-1][1] * cur[-1][2] + int(rng.integers(1, 30)) + c["W"]
+        L = min(L, L_cap)
+        B = int(rng.integers(0, L - c["W"] + 1))
+        case, states = run_case(f"random trajectory {seed} step {step}", c["H"], c["G"], c["d"],
+                                c["W"], L, cur, step, B, c["dtype"], c["p"], seed=seed * 10 + step,
+                                L_cap=L_cap, case=case, states=states, per_head=c["per_head"])
