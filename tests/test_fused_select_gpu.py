@@ -167,3 +167,31 @@ def test_fused_ablation_variants(tem, aeb):
     p.n_warmup, p.n_ramp = 0, 0
     steps = [(spans[:f], f, Lp) for f in (2, 3, 4)]
     run_pair(f"{tem}/{aeb}", 28, 28, 4, steps, B=Lp // 4, p=p, seed=19)
+
+
+@pytest.mark.parametrize("seed", range(16))
+def test_fused_random_configurations(seed):
+    """Sixteen seeded draws of layers, subspaces, frames, budget, bins, grid
+    and variants (the wide shape's fused path when the blocks fit one per
+    CU, the queued kernels otherwise)."""
+    rng = np.random.default_rng(500 + seed)
+    G = int(rng.choice([1, 2, 4, 8]))
+    hpg = int(rng.choice([1, 2, 7]))
+    per_head = bool(rng.random() < 0.25) and G * hpg <= 64
+    n_layers = int(rng.integers(1, 40))
+    spans, t = [], int(rng.integers(0, 40))
+    for f in range(1, int(rng.integers(1, 5)) + 1):
+        rows, cols = int(rng.integers(2, 60)), int(rng.integers(2, 70))
+        spans.append((t, rows, cols, f))
+        t += rows * cols + int(rng.integers(0, 60))
+    Lp = t + int(rng.integers(1, 80))
+    p = sk.params_default()
+    p.n_bins = int(rng.integers(1, 25))
+    p.grid = int(rng.integers(1, 13))
+    p.tem_decay = sk.TEM_DECAY[str(rng.choice(list(sk.TEM_DECAY)))]
+    p.aeb_mode = sk.AEB_MODE[str(rng.choice(list(sk.AEB_MODE)))]
+    if rng.random() < 0.5:
+        p.n_warmup, p.n_ramp = 0, 0
+    steps = [(spans[:f], f, Lp) for f in range(1, len(spans) + 1)]
+    run_pair(f"random {seed}", n_layers, G * hpg, G, steps, B=int(rng.integers(0, Lp + 1)),
+             p=p, per_head=per_head, seed=seed)
