@@ -50,7 +50,7 @@ def run_pair(tag, n_layers, H, G, steps, B, p=None, per_head=False, spoil_layer=
     dims = sk.make_dims(n_layers, H, G, 64, Lp + W, W, sk.BF16, per_head=per_head)
     Ns = H if per_head else G
     p = p or sk.params_default()
-    cap = max(s[1] * s[2] for spans, _, _ in steps for s in spans)
+    cap = max([s[1] * s[2] for spans, _, _ in steps for s in spans] + [1])
     dev = torch.device("cuda:0")
     states = [torch.empty(sk.state_bytes(dims, cap), dtype=torch.uint8, device=dev)
               for _ in range(2)]
@@ -195,3 +195,9 @@ def test_fused_random_configurations(seed):
     steps = [(spans[:f], f, Lp) for f in range(1, len(spans) + 1)]
     run_pair(f"random {seed}", n_layers, G * hpg, G, steps, B=int(rng.integers(0, Lp + 1)),
              p=p, per_head=per_head, seed=seed)
+
+
+def test_fused_no_visual_tokens():
+    """No spans (a text-only context): the statistics have no visual keys
+    and no current frame; the selection applies no discount."""
+    run_pair("no spans", 12, 12, 4, [([], 0, 3000)] * 2, B=600, seed=23)
