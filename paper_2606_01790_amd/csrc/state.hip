@@ -40,6 +40,7 @@
 
 #include "device_common.h"
 #include "grid_cell.h"
+#include "stats_shape.h"
 #include "internal.h"
 #include "select_body.h"
 
@@ -104,14 +105,11 @@ struct StatsShape<1024> {
   static constexpr int kHistInts = 16384, kKeyCache = 20 * 1024, kCand = 2048,
                        kJointOff = 8192, kMaxTies = 63;
 };
-constexpr int kNarrowMaxBins = 17;
 template <>
 struct StatsShape<512> {
   static constexpr int kHistInts = 4096 + kNarrowMaxBins * 256, kKeyCache = 6 * 1024,
                        kCand = 1024, kJointOff = 4096, kMaxTies = kNarrowMaxBins - 1;
 };
-constexpr int kSmallMaxBins = 9;
-constexpr int kSmallMaxCells = 64;
 template <>
 struct StatsShape<256> {
   static constexpr int kHistInts = 4096 + kSmallMaxBins * kSmallMaxCells, kKeyCache = 2048,
@@ -1138,22 +1136,15 @@ void set_wide_lds_attributes() {
   (void)attr_sel;
 }
 
-// The statistics block shape (threads per block) for this call: the wide
-// one when the blocks all fit on the GPU at once (one per CU) or the bins
-// need it, else the narrow one (two per CU), or the small one (four per CU)
-// when even two per CU leave blocks for a second round and the bins and
-// cells allow it; -1 when the device cannot be queried.
+// The statistics block shape for this call (stats_shape.h); -1 when the
+// device cannot be queried.
 int stats_shape(const Geometry& g, const starkv_params& p) {
   int dev = 0, n_cu = 0;
   if (hipGetDevice(&dev) != hipSuccess ||
       hipDeviceGetAttribute(&n_cu, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
       n_cu <= 0)
     return -1;
-  const long blocks = (long)(g.Ns + 2) * g.n_layers;
-  if (blocks <= n_cu || p.n_bins > kNarrowMaxBins) return 1024;
-  if (blocks > 2L * n_cu && p.n_bins <= kSmallMaxBins && p.grid * p.grid <= kSmallMaxCells)
-    return 256;
-  return 512;
+  return stats_shape_for((long)(g.Ns + 2) * g.n_layers, n_cu, p.n_bins, p.grid);
 }
 
 }  // namespace

@@ -6,6 +6,8 @@
 2. The spatial-cell arithmetic of the statistics kernel (grid_cell.h, the
    same source the kernel compiles) against exact integer arithmetic, up to
    the largest frames the boundary accepts (rows * cols <= 2^26).
+3. The statistics kernel's block-shape choice (stats_shape.h) on the
+   workloads' shapes and around every threshold.
 """
 
 import os
@@ -92,3 +94,34 @@ def test_small_quotient_exact_near_every_multiple(tmp_path):
     assert r.returncode == 0, r.stderr
     bad, checked = map(int, r.stdout.split())
     assert checked > 10**6 and bad == 0, (bad, checked)
+
+
+def test_statistics_block_shape(tmp_path):
+    """Wide (1024) when every block fits one per CU or the bins need it;
+    small (256) when even two per CU leave a second round and K <= 9,
+    M*M <= 64; narrow (512) otherwise."""
+    exe = _build(tmp_path, "stats_shape", [os.path.join(HOST, "stats_shape_driver.cpp")],
+                 sanitize=False)
+    cases = [
+        # (blocks, CUs, K, M) -> shape
+        ((28 * 6, 256, 8, 8), 1024),      # 28 layers, 4 groups: the five-frame trajectory
+        ((28 * 30, 256, 8, 8), 256),      # per-head subspaces
+        ((28 * 30, 256, 12, 8), 512),     # per-head, more bins than the small shape holds
+        ((28 * 30, 256, 8, 9), 512),      # per-head, more cells than the small shape holds
+        ((28 * 30, 256, 18, 8), 1024),    # more bins than the narrow shape holds
+        ((48 * 6, 256, 8, 8), 512),       # between one and two blocks per CU
+        ((96 * 6, 256, 9, 8), 256),
+        ((96 * 6, 256, 10, 8), 512),
+        ((96 * 6, 256, 8, 16), 512),
+        ((256, 256, 17, 16), 1024),       # exactly one per CU
+        ((257, 256, 17, 16), 512),
+        ((512, 256, 9, 8), 512),          # exactly two per CU
+        ((513, 256, 9, 8), 256),
+        ((513, 256, 1, 1), 256),
+        ((1, 1, 64, 16), 1024),
+    ]
+    inp = "".join(f"{b} {c} {k} {m}\n" for (b, c, k, m), _ in cases)
+    r = subprocess.run([exe], input=inp, capture_output=True, text=True, timeout=60)
+    assert r.returncode == 0, r.stderr
+    got = [int(x) for x in r.stdout.split()]
+    assert got == [want for _, want in cases], list(zip(cases, got))

@@ -43,9 +43,11 @@ needs_hipcc = pytest.mark.skipif(not (os.path.exists(B.HIPCC) or shutil.which("h
 
 def _shape(src: str, nt: int) -> int:
     """Dynamic LDS bytes of the statistics kernel's block shape `nt`, from
-    the StatsShape specialisation in the source."""
+    the StatsShape specialisation in the source (constants from the source
+    and from stats_shape.h)."""
     consts = {m.group(1): int(m.group(2))
-              for m in re.finditer(r"constexpr int (k\w+) = (\d+);", src)}
+              for m in re.finditer(r"constexpr int (k\w+) = (\d+);",
+                                   src + open(os.path.join(B.CSRC, "stats_shape.h")).read())}
     body = src.split("struct StatsShape<%d> {" % nt, 1)[1].split("};", 1)[0]
 
     def value(name):
