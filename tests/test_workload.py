@@ -150,3 +150,25 @@ def test_bench_roofline_bound_follows_intensity():
         else:
             assert r["unit"] == "GB/s" and abs(r["achieved"] - b / 1e-3 / 1e9) < 0.1
     assert bench.roofline_of(1.0, 1, 10 ** 6, "f32")["peak"] == 157.3
+
+
+def test_bench_fused_call_bytes_and_traffic_guard(tmp_path, monkeypatch):
+    """The fused statistics-and-selection call is credited with the bytes of
+    the two calls it replaces; a traffic summary is used only while the
+    scoring sources hash to the version it was taken on."""
+    import bench
+    spec = WL.SPECS[3]
+    for s in range(1, spec.steps + 1):
+        assert bench.call_bytes(spec, s, "update_state_select") == (
+            bench.call_bytes(spec, s, "update_state") + bench.call_bytes(spec, s, "select"))
+    wl = spec.name
+    prof = tmp_path / "profiles"
+    prof.mkdir()
+    f = prof / f"starkv_score-{wl}.traffic.md"
+    f.write_text("- traffic_bytes_per_launch: 123\n- sources_sha1: abc\n")
+    monkeypatch.setattr(bench, "ROOT", str(tmp_path))
+    monkeypatch.setattr(bench, "sources_sha1", lambda call: "abc")
+    assert bench.measured_traffic("starkv_score", wl) == 123
+    f.write_text("- traffic_bytes_per_launch: 123\n- sources_sha1: 0000\n")
+    assert bench.measured_traffic("starkv_score", wl) is None
+    assert bench.measured_traffic("starkv_compact", wl) is None
