@@ -10,9 +10,10 @@ Every function cites the passage of the paper it follows (section, equation
 or algorithm).  Where the paper is silent or ambiguous, the reading taken is
 stated in the function's docstring.
 
-Parity unpinned: the absolute values of MI, w, phi and s on random inputs
-are pinned only through the invariants and closed forms the tests check;
-beyond those the oracle itself is the reference.
+Every function is tied by at least one CPU test to a fact outside the
+oracle (a closed form, an invariant, a special case that reduces to a
+library routine, brute force on tiny inputs, or a hand-written table), and
+the planted-mistake tests show that each such pin catches a plausible error.
 """
 
 from .starkv_oracle import (  # noqa: F401

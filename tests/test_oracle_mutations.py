@@ -273,6 +273,12 @@ def _confidence_reversed_t(sbar, t_min, t_max, eps):
     return u, t_min + (t_max - t_min) * (1.0 - u)
 
 
+def _aeb_swapped(sbar, params):
+    if params.aeb_mode == "entropy":
+        return O.confidence_temperature(sbar, params.t_min, params.t_max, params.eps)
+    return O.entropy_temperature(sbar, params.t_min, params.t_max, params.eps)
+
+
 def _lambda_ramp_long(n, lam, n_warmup, n_ramp):
     if n <= n_warmup:
         return 0.0
@@ -375,6 +381,8 @@ MUTANTS = [
     ("confidence_temperature", _confidence_reversed_t, "confidence temperature runs the wrong way",
      ["test_confidence_temperature_ends_and_scale_invariance"]),
     ("lambda_schedule", _lambda_ramp_long, "ramp one step too long", ["test_lambda_schedule_values"]),
+    ("aeb_temperature", _aeb_swapped, "AEB variants dispatched the wrong way round",
+     ["test_aeb_temperature_closed_forms_per_variant"]),
     ("gather_compact", _gather_window_from_start, "window rows taken from the cache start",
      ["test_gather_compact_is_row_copy"]),
     ("compress_layer", _compress_window_in_softmax, "window keys inside the softmax",

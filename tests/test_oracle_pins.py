@@ -670,3 +670,20 @@ def test_confidence_temperature_ends_and_scale_invariance():
     assert a[0] == pytest.approx(b[0], rel=1e-12)
     p = r / r.sum()
     assert a[0] == pytest.approx(1.0 - (p.max() - 1 / 300) / (1 - 1 / 300), rel=1e-12)
+
+
+def test_aeb_temperature_closed_forms_per_variant():
+    """s̄ = (1, 1, 2): p = (1/4, 1/4, 1/2).  Entropy variant (sec. 3.6):
+    H^ = (ln 4 / 2 + ln 2 / 2) / ln 3; confidence variant (sec. 4.2 ablation,
+    the reading documented with it): c = (1/2 - 1/3) / (1 - 1/3) = 1/4, so the
+    statistic is 3/4.  T = T_min + (T_max - T_min) x statistic in both; an
+    unknown variant is rejected."""
+    sbar = np.array([1.0, 1.0, 2.0])
+    h = (0.5 * math.log(4.0) + 0.5 * math.log(2.0)) / math.log(3.0)
+    for mode, stat in (("entropy", h), ("confidence", 0.75)):
+        p = O.Params(t_min=0.8, t_max=1.3, eps=0.0, aeb_mode=mode)
+        u, T = O.aeb_temperature(sbar, p)
+        assert u == pytest.approx(stat, rel=1e-12), mode
+        assert T == pytest.approx(0.8 + 0.5 * stat, rel=1e-12), mode
+    with pytest.raises(ValueError):
+        O.aeb_temperature(sbar, O.Params(aeb_mode="peak"))
