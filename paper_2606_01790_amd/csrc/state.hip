@@ -1,14 +1,14 @@
 // Online statistics of one step (sec. 3.4-3.6).
 //
-// stats kernel, grid (G + 2, n_layers), 1024 threads (512 or 256 when the
-// blocks outnumber the CUs, see StatsShape), where G is the call's number of
-// scoring subspaces (the KV groups, or the query heads):
-//   block g < G   spatial MI of subspace g (sec. 3.4, Eq. MI);
-//   block G       the AEB statistic of sbar: normalised entropy H^ (sec. 3.6),
-//                 or one minus the normalised peak mass in the confidence
-//                 variant;
-//   block G + 1   stability phi_g of every subspace with the stability-mean
-//                 update (sec. 3.5).
+// stats kernel, grid (G + 1 + ceil(G / 8), n_layers), 1024 threads (512 or
+// 256 when the blocks outnumber the CUs, see StatsShape), where G is the
+// call's number of scoring subspaces (the KV groups, or the query heads):
+//   block g < G       spatial MI of subspace g (sec. 3.4, Eq. MI);
+//   block G           the AEB statistic of sbar: normalised entropy H^
+//                     (sec. 3.6), or one minus the normalised peak mass in
+//                     the confidence variant;
+//   block G + 1 + j   stability phi_g with the stability-mean update
+//                     (sec. 3.5) of subspaces 8j .. 8j + 7.
 // The last block of each layer to finish then runs the layer's finalize in
 // one wave: MI EMA, min-max prior w, lambda schedule, temperature T, state
 // bookkeeping.
@@ -73,6 +73,7 @@ struct StatsArgs {
   size_t state_stride;
   size_t m_off;
   int G, Lp, nbins, grid, cur, frame_cap, sc;
+  int n_stab;             // stability blocks, kStabSubspaces subspaces each
   int aeb;                // starkv_aeb_mode
   float rho_t, eps;
   SpanSet sp;
@@ -245,9 +246,11 @@ __device__ __forceinline__ void stats_body(const StatsArgs& a) {
     return;
   }
 
-  if (g == a.G + 1) {   // ---------------------------------- stability block
+  if (g > a.G) {   // ------------------------------------ stability blocks
+    const int g_lo = (g - a.G - 1) * kStabSubspaces;
+    const int g_hi = min(g_lo + kStabSubspaces, a.G);
     if (a.cur < 0) {
-      for (int j = tid; j < a.G; j += kThreads) scal[STARKV_SCAL_PHI(a.G) + j] = 0.f;
+      for (int j = g_lo + tid; j < g_hi; j += kThreads) scal[STARKV_SCAL_PHI(a.G) + j] = 0.f;
       return;
     }
     char* blk = a.state + (size_t)layer * a.state_stride;
@@ -259,8 +262,8 @@ __device__ __forceinline__ void stats_body(const StatsArgs& a) {
     // each element by one thread), four iterations' loads in flight; a
     // thread's sums keep ascending token order.
     constexpr int kU = 4;
-    for (int g0 = 0; g0 < a.G; g0 += 4) {
-      const int ng = min(4, a.G - g0);
+    for (int g0 = g_lo; g0 < g_hi; g0 += 4) {
+      const int ng = min(4, g_hi - g0);
       double acc[12];
 #pragma unroll
       for (int j = 0; j < 12; ++j) acc[j] = 0.0;
@@ -1041,7 +1044,7 @@ __global__ __launch_bounds__(NT, 1024 / NT) void stats_kernel(StatsArgs a, SelAr
     __syncthreads();
     if (threadIdx.x == 0) {
       __threadfence();
-      last_s = atomicAdd(&hdr->arrive, 1) == a.G + 1;
+      last_s = atomicAdd(&hdr->arrive, 1) == a.G + a.n_stab;
     }
     __syncthreads();
     if (!last_s) return;
@@ -1093,6 +1096,7 @@ StatsArgs make_stats_args(const Geometry& g, const starkv_params& p, const float
   a.cur = current_span(spans, n_spans, frame);
   a.frame_cap = frame_cap;
   a.sc = (int)scalars_count(g.Ns);
+  a.n_stab = stats_stab_blocks(g.Ns);
   a.aeb = p.aeb_mode;
   a.rho_t = p.rho_t;
   a.eps = p.eps;
@@ -1144,7 +1148,7 @@ int stats_shape(const Geometry& g, const starkv_params& p) {
       hipDeviceGetAttribute(&n_cu, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
       n_cu <= 0)
     return -1;
-  return stats_shape_for((long)(g.Ns + 2) * g.n_layers, n_cu, p.n_bins, p.grid);
+  return stats_shape_for((long)stats_layer_blocks(g.Ns) * g.n_layers, n_cu, p.n_bins, p.grid);
 }
 
 }  // namespace
@@ -1160,7 +1164,7 @@ int launch_update_state(const Geometry& g, const starkv_params& p,
   set_wide_lds_attributes();
   const int nt = stats_shape(g, p);
   if (nt < 0) return (int)hipErrorInvalidDevice;
-  const dim3 grid(g.Ns + 2, g.n_layers);
+  const dim3 grid(stats_layer_blocks(g.Ns), g.n_layers);
   SelArgs none{};
   if (nt == 256)
     stats_kernel<256, false><<<grid, 256, stats_lds<256>(), st>>>(a, none);
@@ -1193,7 +1197,8 @@ int launch_update_state_select(const Geometry& g, const starkv_params& p, const 
   fill_sel_args(sel, g, p, sbar, gstar, scalars, spans, n_spans, frame, B, s, idx,
                 (int)std::min<long>({(long)g.Lp, (long)kSelLdsKeys, room}));
   set_wide_lds_attributes();
-  stats_kernel<1024, true><<<dim3(g.Ns + 2, g.n_layers), 1024, stats_lds<1024>(), st>>>(a, sel);
+  stats_kernel<1024, true><<<dim3(stats_layer_blocks(g.Ns), g.n_layers), 1024,
+                             stats_lds<1024>(), st>>>(a, sel);
   return (int)hipGetLastError();
 }
 
