@@ -201,3 +201,13 @@ def test_fused_no_visual_tokens():
     """No spans (a text-only context): the statistics have no visual keys
     and no current frame; the selection applies no discount."""
     run_pair("no spans", 12, 12, 4, [([], 0, 3000)] * 2, B=600, seed=23)
+
+
+@pytest.mark.parametrize("n_layers,H,G", [(10, 18, 9), (8, 32, 16)])
+def test_fused_several_stability_blocks(n_layers, H, G):
+    """9 and 16 subspaces: two stability blocks per layer, the layer's
+    finalize (and then its selection) in whichever block arrives last, still
+    the wide fused shape (120 and 152 blocks)."""
+    spans, Lp = layout(3, 23, 31)
+    steps = [(spans[:f], f, Lp) for f in (2, 3, 3)]
+    run_pair(f"G={G} stability blocks", n_layers, H, G, steps, B=Lp // 5, seed=29 + G)

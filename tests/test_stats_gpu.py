@@ -270,3 +270,22 @@ def test_more_blocks_than_cus(frames, K, M, n_layers):
     p.n_bins, p.grid = K, M
     sbar = rng.uniform(1e-4, 1e-2, Lp).astype(np.float32)
     run_stats(f"{n_layers} layers K{K} M{M} {frames} frames", steps, sbar, spans, frames, p)
+
+
+@pytest.mark.parametrize("G", [8, 9, 17, 64])
+def test_stability_blocks_over_many_subspaces(G):
+    """A layer's stability means are split over ceil(G/8) blocks of eight
+    subspaces: 8 (one block), 9 (the second block holds one subspace), 17
+    and 64 (eight blocks).  Three layers, two steps (the second step's phi
+    reads the means the first wrote), every subspace's MI and phi against
+    the oracle."""
+    rng = np.random.default_rng(900 + G)
+    spans, Lp = layout(2, 23, 31)
+    n_layers = 3
+    steps = []
+    for _ in range(2):
+        S = rng.lognormal(-7, 1.5, (n_layers, G, Lp)).astype(np.float32)
+        S[:, ::3, 1::4] = S[:, ::3, ::4][:, :, :S[:, ::3, 1::4].shape[2]]   # exact ties
+        steps.append(S)
+    sbar = rng.uniform(1e-4, 1e-2, Lp).astype(np.float32)
+    run_stats(f"G={G} stability blocks", steps, sbar, spans, 2, sk.params_default())
