@@ -1,14 +1,19 @@
 // Online statistics of one step (sec. 3.4-3.6).
 //
-// stats kernel, grid (G + 1 + ceil(G / 8), n_layers), 1024 threads (512 or
+// stats kernel, G + 1 + ceil(G / 8) blocks per layer, 1024 threads (512 or
 // 256 when the blocks outnumber the CUs, see StatsShape), where G is the
-// call's number of scoring subspaces (the KV groups, or the query heads):
-//   block g < G       spatial MI of subspace g (sec. 3.4, Eq. MI);
-//   block G           the AEB statistic of sbar: normalised entropy H^
-//                     (sec. 3.6), or one minus the normalised peak mass in
-//                     the confidence variant;
-//   block G + 1 + j   stability phi_g with the stability-mean update
-//                     (sec. 3.5) of subspaces 8j .. 8j + 7.
+// call's number of scoring subspaces (the KV groups, or the query heads).
+// Block g of a layer computes:
+//   g < G       spatial MI of subspace g (sec. 3.4, Eq. MI);
+//   g = G       the AEB statistic of sbar: normalised entropy H^ (sec. 3.6),
+//               or one minus the normalised peak mass in the confidence
+//               variant;
+//   G + 1 + j   stability phi_g with the stability-mean update (sec. 3.5) of
+//               subspaces 8j .. 8j + 7.
+// The grid is one-dimensional with every layer's MI blocks first (layer-
+// major), then the lighter blocks: consecutive workgroups go to different
+// CUs, so when the blocks outnumber the CUs each CU gets nearly the same
+// number of MI blocks.
 // The last block of each layer to finish then runs the layer's finalize in
 // one wave: MI EMA, min-max prior w, lambda schedule, temperature T, state
 // bookkeeping.
@@ -74,6 +79,7 @@ struct StatsArgs {
   size_t m_off;
   int G, Lp, nbins, grid, cur, frame_cap, sc;
   int n_stab;             // stability blocks, kStabSubspaces subspaces each
+  int n_layers;
   int aeb;                // starkv_aeb_mode
   float rho_t, eps;
   SpanSet sp;
@@ -149,8 +155,22 @@ __device__ inline int wave_sum_i(int v) {
   return v;
 }
 
+// Layer and block-of-layer of this workgroup (the grid order above).
+__device__ __forceinline__ void stats_block(const StatsArgs& a, int* layer, int* g) {
+  const int id = blockIdx.x;
+  const int n_mi = a.G * a.n_layers;
+  if (id < n_mi) {
+    *layer = id / a.G;
+    *g = id - *layer * a.G;
+  } else {
+    const int per = 1 + a.n_stab, k = id - n_mi;
+    *layer = k / per;
+    *g = a.G + (k - *layer * per);
+  }
+}
+
 template <int NT>
-__device__ __forceinline__ void stats_body(const StatsArgs& a) {
+__device__ __forceinline__ void stats_body(const StatsArgs& a, int layer, int g) {
   constexpr int kThreads = NT, kWaves = NT / 64;
   constexpr int kHistInts = StatsShape<NT>::kHistInts, kKeyCache = StatsShape<NT>::kKeyCache,
                 kCand = StatsShape<NT>::kCand, kJointOff = StatsShape<NT>::kJointOff;
@@ -181,7 +201,6 @@ __device__ __forceinline__ void stats_body(const StatsArgs& a) {
   __shared__ double red[kWaves];
   __shared__ double red12[kWaves][12];
 
-  const int layer = blockIdx.y, g = blockIdx.x;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   float* scal = a.scal + (size_t)layer * a.sc;
 
@@ -1025,7 +1044,8 @@ template <int NT, bool SEL>
 __global__ __launch_bounds__(NT, 1024 / NT) void stats_kernel(StatsArgs a, SelArgs sel) {
   static_assert(!SEL || NT == kSelThreads, "the selection body needs a 1024-thread block");
   __shared__ int last_s;
-  const int layer = blockIdx.y;
+  int layer, g;
+  stats_block(a, &layer, &g);
   StateHeader* hdr = reinterpret_cast<StateHeader*>(a.state + (size_t)layer * a.state_stride);
   // A state block built for other dimensions (another subspace count or
   // frame capacity, or never initialised) is left untouched: the layer's
@@ -1034,11 +1054,11 @@ __global__ __launch_bounds__(NT, 1024 / NT) void stats_kernel(StatsArgs a, SelAr
   // here races with nothing.  With SEL, block 0 then selects on the NaN
   // scalars, as a separate selection call would.
   if (hdr->magic != kStateMagic || hdr->G != a.G || hdr->frame_cap != a.frame_cap) {
-    if (blockIdx.x != 0) return;
+    if (g != 0) return;
     for (int i = threadIdx.x; i < a.sc; i += NT)
       a.scal[(size_t)layer * a.sc + i] = __builtin_nanf("");
   } else {
-    stats_body<NT>(a);
+    stats_body<NT>(a, layer, g);
     // Thread 0 wrote every value the finalize reads (MI_g or H^); its fence
     // publishes them before it counts the block.
     __syncthreads();
@@ -1097,6 +1117,7 @@ StatsArgs make_stats_args(const Geometry& g, const starkv_params& p, const float
   a.frame_cap = frame_cap;
   a.sc = (int)scalars_count(g.Ns);
   a.n_stab = stats_stab_blocks(g.Ns);
+  a.n_layers = g.n_layers;
   a.aeb = p.aeb_mode;
   a.rho_t = p.rho_t;
   a.eps = p.eps;
@@ -1164,7 +1185,7 @@ int launch_update_state(const Geometry& g, const starkv_params& p,
   set_wide_lds_attributes();
   const int nt = stats_shape(g, p);
   if (nt < 0) return (int)hipErrorInvalidDevice;
-  const dim3 grid(stats_layer_blocks(g.Ns), g.n_layers);
+  const dim3 grid(stats_layer_blocks(g.Ns) * g.n_layers);
   SelArgs none{};
   if (nt == 256)
     stats_kernel<256, false><<<grid, 256, stats_lds<256>(), st>>>(a, none);
@@ -1197,8 +1218,8 @@ int launch_update_state_select(const Geometry& g, const starkv_params& p, const 
   fill_sel_args(sel, g, p, sbar, gstar, scalars, spans, n_spans, frame, B, s, idx,
                 (int)std::min<long>({(long)g.Lp, (long)kSelLdsKeys, room}));
   set_wide_lds_attributes();
-  stats_kernel<1024, true><<<dim3(stats_layer_blocks(g.Ns), g.n_layers), 1024,
-                             stats_lds<1024>(), st>>>(a, sel);
+  stats_kernel<1024, true><<<stats_layer_blocks(g.Ns) * g.n_layers, 1024, stats_lds<1024>(),
+                             st>>>(a, sel);
   return (int)hipGetLastError();
 }
 
