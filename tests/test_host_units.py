@@ -105,10 +105,10 @@ def test_statistics_block_shape(tmp_path):
     cases = [
         # (blocks, CUs, K, M) -> shape
         ((28 * 6, 256, 8, 8), 1024),      # 28 layers, 4 groups: the five-frame trajectory
-        ((28 * 30, 256, 8, 8), 256),      # per-head subspaces
-        ((28 * 30, 256, 12, 8), 512),     # per-head, more bins than the small shape holds
-        ((28 * 30, 256, 8, 9), 512),      # per-head, more cells than the small shape holds
-        ((28 * 30, 256, 18, 8), 1024),    # more bins than the narrow shape holds
+        ((28 * 33, 256, 8, 8), 256),      # per-head subspaces
+        ((28 * 33, 256, 12, 8), 512),     # per-head, more bins than the small shape holds
+        ((28 * 33, 256, 8, 9), 512),      # per-head, more cells than the small shape holds
+        ((28 * 33, 256, 18, 8), 1024),    # more bins than the narrow shape holds
         ((48 * 6, 256, 8, 8), 512),       # between one and two blocks per CU
         ((96 * 6, 256, 9, 8), 256),
         ((96 * 6, 256, 10, 8), 512),
@@ -125,3 +125,12 @@ def test_statistics_block_shape(tmp_path):
     assert r.returncode == 0, r.stderr
     got = [int(x) for x in r.stdout.split()]
     assert got == [want for _, want in cases], list(zip(cases, got))
+    # blocks per layer: one per subspace (MI), one AEB block, and one
+    # stability block per eight subspaces (four groups: 6; 28 heads: 33)
+    subs = [1, 4, 7, 8, 9, 16, 17, 28, 63, 64]
+    r = subprocess.run([exe, "layer"], input="".join(f"{n}\n" for n in subs),
+                       capture_output=True, text=True, timeout=60)
+    assert r.returncode == 0, r.stderr
+    got = [tuple(map(int, line.split())) for line in r.stdout.splitlines()]
+    assert got == [(-(-n // 8), n + 1 - (-n // 8)) for n in subs], list(zip(subs, got))
+    assert got[1][1] == 6 and got[7][1] == 33
