@@ -1059,8 +1059,10 @@ __global__ __launch_bounds__(NT, 1024 / NT) void stats_kernel(StatsArgs a, SelAr
       a.scal[(size_t)layer * a.sc + i] = __builtin_nanf("");
   } else {
     stats_body<NT>(a, layer, g);
-    // Thread 0 wrote every value the finalize reads (MI_g or H^); its fence
-    // publishes them before it counts the block.
+    // Lanes of wave 0 wrote every value the finalize and a fused selection
+    // read from this block (MI_g or H^ by thread 0, phi by the first eight
+    // lanes); thread 0's fence, in that wave, publishes them before it
+    // counts the block.
     __syncthreads();
     if (threadIdx.x == 0) {
       __threadfence();
