@@ -1060,7 +1060,7 @@ __global__ __launch_bounds__(NT, 1024 / NT) void stats_kernel(StatsArgs a, SelAr
   } else {
     stats_body<NT>(a, layer, g);
     // Lanes of wave 0 wrote every value the finalize and a fused selection
-    // read from this block (MI_g or H^ by thread 0, phi by the first eight
+    // read from this block (MI_g or H^ by thread 0, phi by the first four
     // lanes); thread 0's fence, in that wave, publishes them before it
     // counts the block.
     __syncthreads();
