@@ -704,9 +704,8 @@ __device__ __forceinline__ void stats_body(const StatsArgs& a, int layer, int g)
                         (int)(((bucket_bits[dd >> 5] >> (dd & 31)) & 1u) << 8);
           __syncthreads();
           fetch_reset();
-          auto fuse_key = [&](int i, uint32_t key) {
+          auto fuse_key_in = [&](int i, uint32_t key, int cell) {
             const uint32_t d = (key >> shift) & (uint32_t)(nb - 1);
-            const int cell = cell_at(i);
             const int lut = d_lut[d];
             if (lut & 0x100) {
               const int sg = seg_of_bucket(d);
@@ -718,17 +717,35 @@ __device__ __forceinline__ void stats_body(const StatsArgs& a, int layer, int g)
             }
           };
           cell_reset();
-          if (cached) {   // keys in LDS: one copy of the body
+          if (cached) {
+            // keys in LDS: span by span, so that the span's constants are
+            // uniform and a thread's (row, col) only steps inside the span
+            for (int sp = 0; sp < a.sp.n; ++sp) {
+              const int end = a.sp.off[sp + 1];
+              const int rows = a.sp.rows[sp], cols = a.sp.cols[sp];
+              const float rc = __builtin_amdgcn_rcpf((float)cols);
+              const float fr = (float)M * __builtin_amdgcn_rcpf((float)rows), fc = (float)M * rc;
+              const int dq = small_quot(kThreads, cols, rc), dr = kThreads - dq * cols;
+              int r = small_quot(tid, cols, rc);
+              int c = tid - r * cols;
 #pragma unroll 2
-            for (int i = tid; i < N; i += kThreads) fuse_key(i, kc[i]);
+              for (int i = a.sp.off[sp] + tid; i < end; i += kThreads) {
+                fuse_key_in(i, kc[i], grid_cell(r, c, rows, cols, M, fr, fc));
+                c += dr;
+                r += dq;
+                if (c >= cols) { c -= cols; ++r; }
+              }
+            }
           } else {        // kKeyBatch loads in flight
             fetch_reset();
             for (int i0 = tid; i0 < N; i0 += kKeyBatch * kThreads) {
               uint32_t kv[kKeyBatch];
               fetch(i0, kv);
 #pragma unroll
-              for (int u = 0; u < kKeyBatch; ++u)
-                if (i0 + u * kThreads < N) fuse_key(i0 + u * kThreads, kv[u]);
+              for (int u = 0; u < kKeyBatch; ++u) {
+                const int i = i0 + u * kThreads;
+                if (i < N) fuse_key_in(i, kv[u], cell_at(i));
+              }
             }
           }
           __syncthreads();
