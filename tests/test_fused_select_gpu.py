@@ -211,3 +211,11 @@ def test_fused_several_stability_blocks(n_layers, H, G):
     spans, Lp = layout(3, 23, 31)
     steps = [(spans[:f], f, Lp) for f in (2, 3, 3)]
     run_pair(f"G={G} stability blocks", n_layers, H, G, steps, B=Lp // 5, seed=29 + G)
+
+
+def test_fused_sixty_four_spans():
+    """64 frames of 5x6 (the span limit): the selection's discount table
+    holds 64 spans per subspace."""
+    spans, Lp = layout(64, 5, 6, gap=3)
+    steps = [(spans[:f], f, Lp) for f in (63, 64)]
+    run_pair("64 spans", 12, 12, 4, steps, B=Lp // 5, seed=64)

@@ -289,3 +289,32 @@ def test_stability_blocks_over_many_subspaces(G):
         steps.append(S)
     sbar = rng.uniform(1e-4, 1e-2, Lp).astype(np.float32)
     run_stats(f"G={G} stability blocks", steps, sbar, spans, 2, sk.params_default())
+
+
+@pytest.mark.parametrize("mixed", [False, True])
+def test_sixty_four_spans(mixed):
+    """The largest span count the boundary accepts (64): equal 7x9 frames,
+    or frames of mixed shapes from 1x1 to 13x17 with gaps of 0 to 40 text
+    tokens; the keys fit the wide shape's LDS cache, so the joint histogram
+    walks them span by span."""
+    rng = np.random.default_rng(64 + mixed)
+    if mixed:
+        spans, t = [], int(rng.integers(0, 30))
+        for f in range(1, 65):
+            rows, cols = int(rng.integers(1, 14)), int(rng.integers(1, 18))
+            spans.append((t, rows, cols, f))
+            t += rows * cols + int(rng.integers(0, 41))
+        Lp = t + 17
+    else:
+        spans, Lp = layout(64, 7, 9, gap=5)
+    G, n_layers = 4, 3
+    steps = []
+    for _ in range(2):
+        S = rng.lognormal(-7, 1.5, (n_layers, G, Lp)).astype(np.float32)
+        S[:, 1, 2::5] = S[:, 1, 1::5][:, :S[:, 1, 2::5].shape[1]]   # exact ties
+        steps.append(S)
+    sbar = rng.uniform(1e-4, 1e-2, Lp).astype(np.float32)
+    for K, M in [(8, 8), (5, 3)]:
+        p = sk.params_default()
+        p.n_bins, p.grid = K, M
+        run_stats(f"64 spans mixed={mixed} K{K} M{M}", steps, sbar, spans, 64, p)
