@@ -139,7 +139,11 @@ __device__ __forceinline__ void select_body(const SelArgs& a, int layer, SelShar
 
   // ---- 1. fused score; keys order tokens by descending s
   uint32_t lo = 0xFFFFFFFFu, hi = 0u;
-  int cur = 0;   // first span that does not end at or before this thread's token
+  // the first span that does not end at or before this thread's token, and
+  // its bounds (past the last span: none)
+  int cur = 0;
+  int c_start = a.n_spans > 0 ? sp_start[0] : 0x7FFFFFFF;
+  int c_end = a.n_spans > 0 ? sp_end[0] : 0x7FFFFFFF;
   for (int t0 = tid; t0 < a.Lp; t0 += kSelScoreBatch * kSelThreads) {
     float sbv[kSelScoreBatch];
     int gv[kSelScoreBatch];
@@ -156,8 +160,12 @@ __device__ __forceinline__ void select_body(const SelArgs& a, int layer, SelShar
         const int g = min(gv[u], a.G - 1);
         const float beta = beta_s[g];
         float D = 1.0f;
-        while (cur < a.n_spans && sp_end[cur] <= t) ++cur;
-        if (cur < a.n_spans && sp_start[cur] <= t) D = d_tab[g * a.n_spans + cur];
+        while (t >= c_end) {
+          ++cur;
+          c_start = cur < a.n_spans ? sp_start[cur] : 0x7FFFFFFF;
+          c_end = cur < a.n_spans ? sp_end[cur] : 0x7FFFFFFF;
+        }
+        if (t >= c_start) D = d_tab[g * a.n_spans + cur];
         const float sf = fmaxf(sbv[u] * beta * D, 0.0f);
         const float sv = (inv_t == 1.0f || sf == 0.0f) ? sf : exp2f(inv_t * __log2f(sf));
         s_out[t] = sv;
